@@ -1,0 +1,214 @@
+/*
+ * sparrow.h - C ABI of the MI355X (gfx950) sparse-decode attention library.
+ *
+ * One decode step of one attention layer over a paged KV cache, as used by
+ * sparse rollout in Sparrow (arXiv 2606.08446):
+ *
+ *   1. sparrow_page_meta_update   per-page key min/max metadata (the page
+ *                                 landmark scored in Sec. 3.3 / Appendix C),
+ *   2. sparrow_page_score_topk    page scores against the current query, the
+ *                                 per-sequence page budget from the dynamic
+ *                                 sparsity schedule (Sec. 3.2 Method box) and
+ *                                 the block top-k page selection (Sec. 2,
+ *                                 Appendix D: block top-k attention),
+ *   3. sparrow_sparse_decode_attn softmax attention over the selected pages only
+ *                                 (the "sparse, no scoring" term of the sparse
+ *                                 cost model, Eq. sparse-cost),
+ *   4. sparrow_dense_decode_attn  the dense paged decode it is measured against
+ *                                 (Eq. dense-cost).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller.  The library
+ *    allocates nothing, keeps no state between calls and never synchronises:
+ *    each call only validates its host-visible arguments and enqueues kernels
+ *    on `stream` (a hipStream_t passed as void*; NULL = the null stream).
+ *  - Return value: SPARROW_OK (0) or a negative status (see below).  Nothing is
+ *    enqueued when a negative status is returned.  Faults caused by bad device
+ *    contents (for example a block-table entry outside [0, num_phys_pages))
+ *    are the caller's contract and surface at the caller's next synchronisation.
+ *  - bf16 tensors are IEEE bfloat16 bit patterns.  NaN inputs are not supported.
+ *  - Layouts (row-major, no padding):
+ *      q            bf16  [batch][num_q_heads][head_dim]
+ *      k_cache      bf16  [num_phys_pages][num_kv_heads][page_size][head_dim]
+ *      v_cache      bf16  [num_phys_pages][num_kv_heads][page_size][head_dim]
+ *      meta         bf16  [num_phys_pages][num_kv_heads][2][head_dim]
+ *                         (row 0: channel-wise min, row 1: channel-wise max)
+ *      block_table  int32 [batch][max_pages_per_seq]  logical -> physical page
+ *      seq_lens     int32 [batch]  tokens of each sequence, including the token
+ *                                  being decoded (0 allowed)
+ *      idx          int32 [batch][num_kv_heads][k_max]  selected logical pages
+ *      out          fp32 or bf16 [batch][num_q_heads][head_dim]
+ *    Sequence b uses logical pages 0 .. ceil(seq_lens[b] / page_size) - 1;
+ *    only those block-table entries are read.  Query head j reads KV head
+ *    j / G with G = num_q_heads / num_kv_heads (grouped-query attention).
+ *  - Supported shapes: head_dim == 128; page_size in {16, 32, 64, 128};
+ *    num_q_heads a multiple of num_kv_heads with G <= 16;
+ *    1 <= max_pages_per_seq <= SPARROW_MAX_PAGES_PER_SEQ.
+ */
+#ifndef SPARROW_H
+#define SPARROW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPARROW_OK 0
+#define SPARROW_EINVAL (-1)       /* null pointer, negative or inconsistent size      */
+#define SPARROW_EUNSUPPORTED (-2) /* head_dim, page size, group size or dtype not supported */
+#define SPARROW_EWORKSPACE (-3)   /* workspace missing or smaller than required       */
+#define SPARROW_EHIP (-4)         /* a kernel launch failed                           */
+
+#define SPARROW_MAX_PAGES_PER_SEQ 15360
+
+#define SPARROW_OUT_F32 0
+#define SPARROW_OUT_BF16 1
+
+#define SPARROW_OP_SCORE_TOPK 0
+#define SPARROW_OP_SPARSE_ATTN 1
+#define SPARROW_OP_DENSE_ATTN 2
+
+/* Shape of one layer's decode batch (host struct, read during the call only). */
+typedef struct sparrow_shape {
+    int32_t batch;
+    int32_t num_q_heads;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t page_size;
+    int32_t max_pages_per_seq;
+    int64_t num_phys_pages;
+} sparrow_shape_t;
+
+/*
+ * Dynamic sparsity schedule (Sec. 3.2 Method box: the budget grows with the
+ * current length so that the tail acceptance rate stays constant; lengths are
+ * grouped into bins of 2K tokens in the paper).  Host struct whose two tables
+ * are DEVICE arrays of n_bins int32.  For a sequence of L >= 1 tokens and
+ * n = ceil(L / page_size) pages:
+ *     bin = min((L - 1) / bin_tokens, n_bins - 1)
+ *     k   = clamp(max(min_pages[bin], ceil(n * frac_num[bin] / frac_den)), 1, n)
+ * and k = 0 for L = 0.  A fixed budget is min_pages = {P}, frac_num = {0}; a
+ * fixed fraction is min_pages = {0}, frac_num = {num}, frac_den = den.  When
+ * k == n every page is kept (Appendix F: attention is dense while the context
+ * fits the budget).  Requires bin_tokens >= 1, n_bins >= 1, frac_den >= 1 and
+ * non-negative table entries.
+ */
+typedef struct sparrow_schedule {
+    int32_t bin_tokens;
+    int32_t n_bins;
+    const int32_t *min_pages;
+    const int32_t *frac_num;
+    int32_t frac_den;
+} sparrow_schedule_t;
+
+/*
+ * Per-page key metadata (Sec. 3.3 and Appendix C: landmark scores; the
+ * landmark is the channel-wise min and max of the page's keys).
+ *
+ * For every sequence b and every logical page p that overlaps the token range
+ * [first_pos[b], seq_lens[b]), and for every KV head h and channel i:
+ *     meta[phys][h][0][i] = min over the valid tokens t of the page of K[t][i]
+ *     meta[phys][h][1][i] = max over the same tokens
+ * where phys = block_table[b][p] and the valid tokens of page p are
+ * p*page_size .. min((p+1)*page_size, seq_lens[b]) - 1.  Values are copied
+ * exactly (bf16 in, bf16 out); -0 orders below +0.  first_pos == NULL rebuilds
+ * every page of every sequence.  A decode step that has just written token
+ * L-1 passes first_pos[b] = L-1.  Entries of first_pos below 0 are treated as
+ * 0; entries >= seq_lens[b] update nothing.
+ *
+ * Arguments: shape (host), k_cache (device, layout above), block_table,
+ * seq_lens, first_pos (device [batch] or NULL), meta (device, written), stream.
+ * Errors: SPARROW_EINVAL for a null shape/k_cache/block_table/seq_lens/meta or
+ * a bad size; SPARROW_EUNSUPPORTED for head_dim/page_size; SPARROW_EHIP.
+ */
+int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
+                             const int32_t *block_table, const int32_t *seq_lens,
+                             const int32_t *first_pos, void *meta, void *stream);
+
+/*
+ * Page scoring and block top-k selection (Sec. 3.3: landmark scores and top-k
+ * page picking; Sec. 3.2: the budget from the sparsity schedule).
+ *
+ * For every sequence b and KV head h, each logical page p < n_b is scored
+ *     S_h(p) = sum over the G query heads j of head h of
+ *              sum_i max(q[b][j][i] * mn_i(p), q[b][j][i] * mx_i(p))
+ * (an upper bound of q_j . k_t over the tokens of the page), with fp32
+ * arithmetic.  k_b is the schedule's budget (see sparrow_schedule_t), capped
+ * at k_max.  The k_b pages of largest S_h are kept, ties going to the lower
+ * page index (-0 equals +0), and written in ascending page order to
+ * out_idx[b][h][0 .. k_b); the rest of the row up to k_max is set to -1.
+ * out_k[b] = k_b.  When k_b == n_b no page is scored and every page is kept.
+ *
+ * Arguments: shape (host); q, meta, block_table, seq_lens (device);
+ * schedule (host struct with device tables); k_max >= 1 (the row length of
+ * out_idx; callers pass at least the largest budget); out_k (device [batch]);
+ * out_idx (device [batch][num_kv_heads][k_max]); workspace of at least
+ * sparrow_workspace_size(shape, k_max, SPARROW_OP_SCORE_TOPK) bytes (device,
+ * contents need not be initialised); stream.
+ * Errors: SPARROW_EINVAL (null pointers, k_max < 1, bad schedule sizes),
+ * SPARROW_EUNSUPPORTED, SPARROW_EWORKSPACE, SPARROW_EHIP.
+ */
+int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const void *meta,
+                            const int32_t *block_table, const int32_t *seq_lens,
+                            const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
+                            int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Sparse decode attention over the selected pages (block-sparse attention,
+ * Sec. 2; the attention term of Eq. sparse-cost).
+ *
+ * For every sequence b and query head j (KV head h = j / G) the token set T is
+ * the valid tokens of the pages idx[b][h][0 .. min(k[b], k_max)); entries
+ * outside [0, n_b) are skipped.  Then
+ *     z_t = scale * (q[b][j] . K[t]),  w_t = exp(z_t - max z) / sum exp(z - max z)
+ *     out[b][j] = sum_t w_t V[t]
+ * computed with bf16 operands and fp32 accumulation (the softmax weights are
+ * rounded to bf16 before they multiply V).  An empty token set gives a zero
+ * row.  out_dtype is SPARROW_OUT_F32 or SPARROW_OUT_BF16.
+ *
+ * Arguments: shape (host); q, k_cache, v_cache, block_table, seq_lens, k
+ * (device [batch]), idx (device [batch][num_kv_heads][k_max]); k_max >= 1;
+ * scale (typically 1/sqrt(head_dim)); out (device, written); out_dtype;
+ * workspace of at least sparrow_workspace_size(shape, k_max,
+ * SPARROW_OP_SPARSE_ATTN) bytes; stream.
+ * Errors: SPARROW_EINVAL, SPARROW_EUNSUPPORTED, SPARROW_EWORKSPACE, SPARROW_EHIP.
+ */
+int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, const void *k_cache,
+                               const void *v_cache, const int32_t *block_table,
+                               const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
+                               int32_t k_max, float scale, void *out, int32_t out_dtype,
+                               void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Dense paged decode attention (the dense rollout baseline, Eq. dense-cost):
+ * the same as sparrow_sparse_decode_attn with T = every valid token of the
+ * sequence.
+ *
+ * Arguments as above, without k/idx/k_max; workspace of at least
+ * sparrow_workspace_size(shape, 0, SPARROW_OP_DENSE_ATTN) bytes.
+ * Errors: SPARROW_EINVAL, SPARROW_EUNSUPPORTED, SPARROW_EWORKSPACE, SPARROW_EHIP.
+ */
+int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const void *k_cache,
+                              const void *v_cache, const int32_t *block_table,
+                              const int32_t *seq_lens, float scale, void *out, int32_t out_dtype,
+                              void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Workspace bytes needed by one call of `op` (SPARROW_OP_*) with this shape
+ * and k_max (ignored for SPARROW_OP_DENSE_ATTN).  Returns 0 for an invalid or
+ * unsupported shape.  The workspace holds scratch results of one call only;
+ * calls that run concurrently need separate workspaces.
+ */
+size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32_t op);
+
+/* Static, human-readable name of a status code. */
+const char *sparrow_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARROW_H */

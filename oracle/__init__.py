@@ -1,0 +1,185 @@
+"""CPU oracle for Sparrow's sparse-decode step (arXiv 2606.08446).
+
+TEST INFRASTRUCTURE ONLY: the plain C reference in ``sparrow_oracle.c`` behind
+numpy-level wrappers.  Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the GPU library never calls it and
+shares no code with it.
+
+Every function takes numpy arrays: bf16 tensors travel as ``uint16`` bit
+patterns, indices as ``int32``.  Layouts are those of ``sparrow_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+# SPARROW_ORACLE_LIB lets the mutation tests load a deliberately broken build.
+_LIB_PATH = os.environ.get("SPARROW_ORACLE_LIB", os.path.join(_HERE, "liboracle.so"))
+_lib = None
+
+_i32 = ctypes.c_int32
+_p = ctypes.c_void_p
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        subprocess.check_call(["make", "-s", "-C", _HERE])
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.oracle_budget.argtypes = [_i32, _i32, _i32, _i32, _p, _p, _i32]
+    lib.oracle_budget.restype = _i32
+    lib.oracle_budgets.argtypes = [_i32, _p, _i32, _i32, _i32, _p, _p, _i32, _p]
+    lib.oracle_budgets.restype = None
+    lib.oracle_page_meta.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p]
+    lib.oracle_page_meta.restype = None
+    lib.oracle_page_scores.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p,
+                                       _p, _p]
+    lib.oracle_page_scores.restype = None
+    lib.oracle_topk.argtypes = [_p, _i32, _i32, _p]
+    lib.oracle_topk.restype = None
+    lib.oracle_select.argtypes = [_i32, _i32, _i32, _i32, _p, _p, _p, _i32, _p]
+    lib.oracle_select.restype = None
+    lib.oracle_attention.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p,
+                                     _p, _p, _i32, ctypes.c_double, _p]
+    lib.oracle_attention.restype = None
+    lib.oracle_weight_sum.argtypes = [_i32, ctypes.c_int64, _p, _p, ctypes.c_double]
+    lib.oracle_weight_sum.restype = ctypes.c_double
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = _i32
+    _lib = lib
+    return lib
+
+
+def _c(a, dtype):
+    """Contiguous array of ``dtype`` and its address (the array is returned to keep it alive)."""
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def budget(L, ps, bin_tokens, min_pages, frac_num, frac_den) -> int:
+    """Page budget of one sequence of ``L`` tokens (Sec. 3.2 schedule)."""
+    mp, mpp = _c(min_pages, np.int32)
+    fn, fnp = _c(frac_num, np.int32)
+    return int(_load().oracle_budget(int(L), int(ps), int(bin_tokens), len(mp), mpp, fnp,
+                                     int(frac_den)))
+
+
+def budgets(seq_lens, ps, bin_tokens, min_pages, frac_num, frac_den) -> np.ndarray:
+    sl, slp = _c(seq_lens, np.int32)
+    mp, mpp = _c(min_pages, np.int32)
+    fn, fnp = _c(frac_num, np.int32)
+    out = np.zeros(len(sl), np.int32)
+    _load().oracle_budgets(len(sl), slp, int(ps), int(bin_tokens), len(mp), mpp, fnp,
+                           int(frac_den), out.ctypes.data)
+    return out
+
+
+def page_meta(k_cache, block_table, seq_lens, first_pos=None, meta=None) -> np.ndarray:
+    """Min/max key metadata ``[P][Hkv][2][D]`` (uint16 bf16 bits).
+
+    With ``first_pos`` given, only pages overlapping ``[first_pos[b], L_b)`` are
+    recomputed in a copy of ``meta``; otherwise every page is built."""
+    P, Hkv, ps, D = k_cache.shape
+    B, max_pages = block_table.shape
+    kc, kcp = _c(k_cache, np.uint16)
+    bt, btp = _c(block_table, np.int32)
+    sl, slp = _c(seq_lens, np.int32)
+    if meta is None:
+        out = np.zeros((P, Hkv, 2, D), np.uint16)
+    else:
+        out = np.array(meta, dtype=np.uint16, copy=True, order="C")
+    fp_arr, fpp = (None, None) if first_pos is None else _c(first_pos, np.int32)
+    _load().oracle_page_meta(B, Hkv, D, ps, max_pages, kcp, btp, slp, fpp, out.ctypes.data)
+    return out
+
+
+def page_scores(q, meta, block_table, seq_lens, ps):
+    """(scores32, scores64), each ``[B][Hkv][max_pages]``; entries past ``n_b`` are NaN."""
+    B, Hq, D = q.shape
+    P, Hkv, _, _ = meta.shape
+    max_pages = block_table.shape[1]
+    qq, qp = _c(q, np.uint16)
+    mm, mp = _c(meta, np.uint16)
+    bt, btp = _c(block_table, np.int32)
+    sl, slp = _c(seq_lens, np.int32)
+    s32 = np.full((B, Hkv, max_pages), np.nan, np.float32)
+    s64 = np.full((B, Hkv, max_pages), np.nan, np.float64)
+    _load().oracle_page_scores(B, Hq, Hkv, D, ps, max_pages, qp, mp, btp, slp,
+                               s32.ctypes.data, s64.ctypes.data)
+    return s32, s64
+
+
+def topk(scores, k) -> np.ndarray:
+    """Indices of the ``k`` largest scores (ties to the lower index), ascending."""
+    s, sp = _c(scores, np.float32)
+    k = min(int(k), len(s))
+    out = np.zeros(max(k, 0), np.int32)
+    _load().oracle_topk(sp, len(s), k, out.ctypes.data)
+    return out
+
+
+def select(seq_lens, k_of_seq, scores32, ps, k_max) -> np.ndarray:
+    """Top-k page lists ``[B][Hkv][k_max]`` (ascending, padded with -1)."""
+    B, Hkv, max_pages = scores32.shape
+    sl, slp = _c(seq_lens, np.int32)
+    kk, kp = _c(k_of_seq, np.int32)
+    s, sp = _c(scores32, np.float32)
+    idx = np.zeros((B, Hkv, k_max), np.int32)
+    _load().oracle_select(B, Hkv, ps, max_pages, slp, kp, sp, int(k_max), idx.ctypes.data)
+    return idx
+
+
+def attention(q, k_cache, v_cache, block_table, seq_lens, scale, k_of_seq=None, idx=None):
+    """fp64 attention output ``[B][Hq][D]``; dense when ``idx`` is None."""
+    B, Hq, D = q.shape
+    P, Hkv, ps, _ = k_cache.shape
+    max_pages = block_table.shape[1]
+    qq, qp = _c(q, np.uint16)
+    kc, kcp = _c(k_cache, np.uint16)
+    vc, vcp = _c(v_cache, np.uint16)
+    bt, btp = _c(block_table, np.int32)
+    sl, slp = _c(seq_lens, np.int32)
+    out = np.zeros((B, Hq, D), np.float64)
+    if idx is None:
+        kp = ip = None
+        k_max = 0
+    else:
+        kk, kp = _c(k_of_seq, np.int32)
+        ii, ip = _c(idx, np.int32)
+        k_max = ii.shape[2]
+    _load().oracle_attention(B, Hq, Hkv, D, ps, max_pages, qp, kcp, vcp, btp, slp, kp, ip,
+                             int(k_max), float(scale), out.ctypes.data)
+    return out
+
+
+def weight_sum(qj, keys, scale) -> float:
+    """Sum of the softmax weights of one query over ``keys`` ``[n][D]``."""
+    qq, qp = _c(qj, np.uint16)
+    kk, kp = _c(keys, np.uint16)
+    return float(_load().oracle_weight_sum(kk.shape[1], kk.shape[0], qp, kp, float(scale)))
+
+
+def sparse_step(q, k_cache, v_cache, block_table, seq_lens, schedule, k_max, scale):
+    """The whole sparse step on the CPU: meta, scores, budget, top-k, attention.
+
+    ``schedule`` is ``(bin_tokens, min_pages, frac_num, frac_den)``.
+    Returns a dict with every intermediate."""
+    ps = k_cache.shape[2]
+    bin_tokens, min_pages, frac_num, frac_den = schedule
+    meta = page_meta(k_cache, block_table, seq_lens)
+    s32, s64 = page_scores(q, meta, block_table, seq_lens, ps)
+    k = budgets(seq_lens, ps, bin_tokens, min_pages, frac_num, frac_den)
+    k = np.minimum(k, k_max).astype(np.int32)
+    idx = select(seq_lens, k, s32, ps, k_max)
+    out = attention(q, k_cache, v_cache, block_table, seq_lens, scale, k, idx)
+    return {"meta": meta, "scores32": s32, "scores64": s64, "k": k, "idx": idx, "out": out}

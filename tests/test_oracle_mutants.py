@@ -1,0 +1,60 @@
+"""The oracle pins must catch plausible mistakes in the oracle.
+
+Each case plants one mistake in a copy of ``oracle/sparrow_oracle.c`` (on the
+CPU, in a temporary directory), builds it, and runs the pin suite against the
+broken build in a child process; the suite has to fail.
+"""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "sparrow_oracle.c")
+
+MUTANTS = {
+    "topk_ties_to_higher_index": ("return (a->p > b->p) - (a->p < b->p);",
+                                  "return (a->p < b->p) - (a->p > b->p);"),
+    "score_min_instead_of_max": ("s32 += lo > hi ? lo : hi;", "s32 += lo < hi ? lo : hi;"),
+    "score_max_row_is_min_row": ("const uint16_t *mx = mn + D;", "const uint16_t *mx = mn;"),
+    "attention_drops_scale": ("z[n_tok] = scale * dot;", "z[n_tok] = dot;"),
+    "attention_reads_past_length": (
+        "                int64_t t_end = L - p * ps < ps ? L - p * ps : ps;\n"
+        "                for (int64_t t = 0; t < t_end; ++t) {\n"
+        "                    const uint16_t *kt",
+        "                int64_t t_end = L - p * ps < ps ? L - p * ps + 1 : ps;\n"
+        "                for (int64_t t = 0; t < t_end; ++t) {\n"
+        "                    const uint16_t *kt"),
+    "attention_values_from_keys": (
+        "const uint16_t *vt = v_cache + ", "const uint16_t *vt = k_cache + "),
+    "meta_skips_last_token": ("for (int64_t t = 1; t < t_end; ++t) {\n                        uint16_t v",
+                              "for (int64_t t = 1; t < t_end - 1; ++t) {\n                        uint16_t v"),
+    "meta_ignores_signed_zero_order": ("if (a == b && (a_bits & 0x8000u) && !(b_bits & 0x8000u))",
+                                       "if (0)"),
+    "budget_floor_instead_of_ceil": ("(n * (int64_t)frac_num[bin] + frac_den - 1) / frac_den",
+                                     "(n * (int64_t)frac_num[bin]) / frac_den"),
+    "budget_bin_off_by_one": ("int64_t bin = (int64_t)(L - 1) / bin_tokens;",
+                              "int64_t bin = (int64_t)L / bin_tokens;"),
+    "budget_no_page_clamp": ("    if (k > n)\n        k = n;\n    return (int32_t)k;",
+                             "    return (int32_t)k;"),
+    "select_pads_with_zero": ("row[i] = -1;", "row[i] = 0;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    mutant = tmp_path / "sparrow_oracle.c"
+    mutant.write_text(src.replace(old, new))
+    lib = tmp_path / "liboracle_mutant.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-fopenmp", "-ffp-contract=off",
+                           "-shared", "-o", str(lib), str(mutant), "-lm"])
+    env = dict(os.environ, SPARROW_ORACLE_LIB=str(lib), OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
