@@ -1,0 +1,322 @@
+"""Benchmark of the sparse decode step on one MI355X.
+
+One step = one decode step of one attention layer for the whole batch:
+metadata update of the page holding each sequence's newest token, page
+scoring + budget + top-k, sparse attention over the selected pages (split-KV
+and combine).  The dense paged decode over the same cache is timed beside it.
+Inputs are resident in HBM before the timed region starts.
+
+Prints ONE JSON line.  ``value`` is decode queries per second per layer
+(batch / step time).  ``roofline`` reports the dominant entry point's
+algorithmic bytes per launch over its average duration (HIP events on the
+stream the kernels are launched on) against the 8 TB/s HBM peak.
+``cpu_baseline`` times the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sparse decode attn queries/sec per layer + achieved HBM GB/s (% of peak) vs dense"
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_attn.txt")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c2", help="c1..c5, or c4-2/c4-5/c4-10/c4-25/c4-100")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (for counter scaling)")
+    return ap.parse_args()
+
+
+def workload(name):
+    from paper_2606_08446_amd import workloads as W
+    if name.startswith("c4-"):
+        pct = {"2": 0, "5": 1, "10": 2, "25": 3, "100": 4}[name.split("-")[1]]
+        return W.c4_with_fraction(pct)
+    return W.CONFIGS[name]
+
+
+def sparse_bytes(inp, k_host, idx_host):
+    """Algorithmic HBM bytes of one sparse step, per phase."""
+    import numpy as np
+    w = inp.workload
+    ps, Hkv, Hq, D = w.page_size, w.num_kv_heads, w.num_q_heads, 128
+    lens = inp.lens_host
+    meta_update = 0
+    score = 0
+    kv = 0
+    for b, L in enumerate(lens):
+        L = int(L)
+        if L <= 0:
+            continue
+        n = -(-L // ps)
+        last_valid = L - (n - 1) * ps
+        meta_update += Hkv * (last_valid * D * 2 + 2 * D * 2)       # read page keys, write meta
+        k = int(k_host[b])
+        if k < n:
+            score += Hkv * n * 2 * D * 2                              # meta rows
+        for h in range(Hkv):
+            sel = idx_host[b, h, :k]
+            toks = k * ps - (ps - last_valid if (n - 1) in set(sel.tolist()) else 0)
+            kv += toks * 2 * D * 2                                    # K and V rows
+    q_out = len(lens) * Hq * D * (2 + 4)
+    return {"meta_update": meta_update, "score_topk": score + len(lens) * Hq * D * 2,
+            "sparse_attn": kv + q_out}
+
+
+def dense_bytes(inp):
+    w = inp.workload
+    return int(sum(int(L) for L in inp.lens_host)) * w.num_kv_heads * 2 * 128 * 2 + \
+        len(inp.lens_host) * w.num_q_heads * 128 * (2 + 4)
+
+
+def read_traffic(kernel_src_sha):
+    """HBM traffic per launch from the committed counter summary, if it matches the source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != kernel_src_sha or "traffic_bytes_per_launch" not in vals:
+        return None
+    return float(vals["traffic_bytes_per_launch"])
+
+
+def source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("attention.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2606_08446_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def cpu_baseline(inp, k_max, target_s):
+    """The oracle's sparse step on a sample of sequences, repeated to ~target_s seconds."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2606_08446_amd import workloads as W
+    w = inp.workload
+    s = w.schedule
+    ps = w.page_size
+    B = w.batch
+    n_seq = min(B, 8)
+    seqs = list(range(n_seq))
+    bt_all = inp.block_table.cpu().numpy()
+    phys, rows = [], []
+    for b in seqs:
+        n = -(-int(inp.lens_host[b]) // ps)
+        rows.append(len(phys))
+        phys.extend(int(x) for x in bt_all[b, :n])
+    max_n = max(1, max(-(-int(inp.lens_host[b]) // ps) for b in seqs))
+    bt = np.zeros((n_seq, max_n), np.int32)
+    for i, b in enumerate(seqs):
+        n = -(-int(inp.lens_host[b]) // ps)
+        bt[i, :n] = np.arange(rows[i], rows[i] + n)
+    pi = torch.as_tensor(np.array(phys, np.int64), device=inp.k_cache.device)
+    q = W.bf16_bits(inp.q[:n_seq])
+    kc = W.bf16_bits(inp.k_cache[pi])
+    vc = W.bf16_bits(inp.v_cache[pi])
+    lens = inp.lens_host[:n_seq].astype(np.int32)
+    meta = oracle.page_meta(kc, bt, lens)       # setup: metadata before the step
+    first = (lens - 1).astype(np.int32)
+    scale = 1.0 / math.sqrt(128.0)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        m2 = oracle.page_meta(kc, bt, lens, first_pos=first, meta=meta)
+        s32, _ = oracle.page_scores(q, m2, bt, lens, ps)
+        k = np.minimum(oracle.budgets(lens, ps, s.bin_tokens, s.min_pages, s.frac_num,
+                                      s.frac_den), k_max).astype(np.int32)
+        idx = oracle.select(lens, k, s32, ps, k_max)
+        oracle.attention(q, kc, vc, bt, lens, scale, k, idx)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s:
+            break
+    return {"value": round(n_seq * reps / el, 3), "unit": "queries/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"first {n_seq} of {B} sequences of {w.name}, whole sparse step "
+                      f"(metadata update of the newest page, fp32+fp64 scores, budget, top-k, "
+                      f"fp64 attention) repeated {reps}x in {el:.1f} s"}
+
+
+def copy_calibration():
+    """A plain device-to-device copy of known size, for scaling the HBM counters."""
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_each_way": n, "launches": 5}), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sparse decode "
+              "path has no multi-GPU mode in this build.", file=sys.stderr, flush=True)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import numpy as np
+    import torch
+
+    from paper_2606_08446_amd import sparrow as S
+    from paper_2606_08446_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = workload(args.workload)
+    inp = W.generate(w, dev)
+    s = w.schedule
+    k_max = S.budget_bound(inp.lens_host, w.page_size, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den)
+    meta = torch.zeros((inp.num_phys_pages, w.num_kv_heads, 2, 128), dtype=torch.bfloat16,
+                       device=dev)
+    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta)
+    step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+                              meta, inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, k_max)
+    first_pos = (inp.seq_lens - 1).clamp(min=0)
+    dense_out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
+    dense_ws = torch.empty(max(16, S.sparrow_workspace_size(step.shape, 0,
+                                                            S.SPARROW_OP_DENSE_ATTN)),
+                           dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    sp = stream.cuda_stream
+
+    def dense_call():
+        S._check("sparrow_dense_decode_attn", S.sparrow_dense_decode_attn(
+            step.shape, inp.q.data_ptr(), inp.k_cache.data_ptr(), inp.v_cache.data_ptr(),
+            inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), step.scale,
+            dense_out.data_ptr(), S.SPARROW_OUT_F32, dense_ws.data_ptr(), dense_ws.numel(), sp))
+
+    for _ in range(args.warmup):
+        step.meta_update(first_pos, sp)
+        step.score_topk(sp)
+        step.attend(sp)
+        dense_call()
+    torch.cuda.synchronize()
+
+    # ---- timed sparse steps (events between the three entry points, on the same stream)
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(K):
+        ev[i][0].record(stream)
+        step.meta_update(first_pos, sp)
+        ev[i][1].record(stream)
+        step.score_topk(sp)
+        ev[i][2].record(stream)
+        step.attend(sp)
+        ev[i][3].record(stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(stop)
+    phase = {"meta_update": 0.0, "score_topk": 0.0, "sparse_attn": 0.0}
+    for e in ev:
+        phase["meta_update"] += e[0].elapsed_time(e[1])
+        phase["score_topk"] += e[1].elapsed_time(e[2])
+        phase["sparse_attn"] += e[2].elapsed_time(e[3])
+    phase = {k: v / K for k, v in phase.items()}
+    ms_step = total_ms / K
+
+    # ---- timed dense steps
+    dstart = torch.cuda.Event(enable_timing=True)
+    dstop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    dstart.record(stream)
+    for _ in range(K):
+        dense_call()
+    dstop.record(stream)
+    torch.cuda.synchronize()
+    ms_dense = dstart.elapsed_time(dstop) / K
+
+    k_host = step.k.cpu().numpy()
+    idx_host = step.idx.cpu().numpy()
+    by = sparse_bytes(inp, k_host, idx_host)
+    total_bytes = sum(by.values())
+    dbytes = dense_bytes(inp)
+    B = w.batch
+    gbps = total_bytes / (ms_step * 1e-3) / 1e9
+    dgbps = dbytes / (ms_dense * 1e-3) / 1e9
+    dominant = max(phase, key=phase.get)
+    dom_gbps = by[dominant] / (phase[dominant] * 1e-3) / 1e9
+    traffic = read_traffic(source_sha()) if dominant == "sparse_attn" else None
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(inp, k_max, args.cpu_seconds)
+
+    budgets = np.asarray(k_host)
+    result = {
+        "metric": METRIC,
+        "value": round(B / (ms_step * 1e-3), 2),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "num_q_heads": w.num_q_heads,
+                   "num_kv_heads": w.num_kv_heads, "head_dim": 128, "page_size": w.page_size,
+                   "len_range": [w.len_lo, w.len_hi], "budget_pages": [int(budgets.min()),
+                                                                       int(budgets.max())],
+                   "k_max": int(k_max)},
+        "achieved_GBps": round(gbps, 1),
+        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "algorithmic_bytes_per_step": {k: int(v) for k, v in by.items()},
+        "phase_ms": {k: round(v, 5) for k, v in phase.items()},
+        "dense": {"queries_per_s": round(B / (ms_dense * 1e-3), 2), "ms_per_step": round(ms_dense, 5),
+                  "bytes_per_step": int(dbytes), "achieved_GBps": round(dgbps, 1),
+                  "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4)},
+        "speedup_vs_dense": round(ms_dense / ms_step, 3),
+        "roofline": {"kernel": {"sparse_attn": "k_attn_split<sparse> + k_combine",
+                                "score_topk": "k_page_score + k_topk",
+                                "meta_update": "k_meta_update"}[dominant],
+                     "bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+        "wall_s_timed": round(wall, 3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,156 @@
+// C ABI of libsparrow: argument validation, workspace sizing and kernel launches.
+// Declarations and the contract of every entry point are in include/sparrow.h.
+#include "common.h"
+
+using namespace sparrow;
+
+namespace {
+
+int check_shape(const sparrow_shape_t *s)
+{
+    if (!s)
+        return SPARROW_EINVAL;
+    if (s->batch < 0 || s->num_q_heads < 1 || s->num_kv_heads < 1 || s->max_pages_per_seq < 1 ||
+        s->num_phys_pages < 1)
+        return SPARROW_EINVAL;
+    if (s->num_q_heads % s->num_kv_heads != 0)
+        return SPARROW_EINVAL;
+    if (s->num_q_heads / s->num_kv_heads > 16)
+        return SPARROW_EUNSUPPORTED;
+    if (s->head_dim != kHeadDim)
+        return SPARROW_EUNSUPPORTED;
+    if (s->page_size != 16 && s->page_size != 32 && s->page_size != 64 && s->page_size != 128)
+        return SPARROW_EUNSUPPORTED;
+    if (s->max_pages_per_seq > SPARROW_MAX_PAGES_PER_SEQ)
+        return SPARROW_EUNSUPPORTED;
+    if ((int64_t)s->batch * s->num_q_heads > 0x7fffffff / kHeadDim)
+        return SPARROW_EINVAL;
+    return SPARROW_OK;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? SPARROW_OK : SPARROW_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
+                             const int32_t *block_table, const int32_t *seq_lens,
+                             const int32_t *first_pos, void *meta, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!k_cache || !block_table || !seq_lens || !meta)
+        return SPARROW_EINVAL;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    if (first_pos == nullptr && shape->batch > 65535)
+        return SPARROW_EINVAL;
+    return status_of(launch_meta_update(*shape, k_cache, block_table, seq_lens, first_pos, meta,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const void *meta,
+                            const int32_t *block_table, const int32_t *seq_lens,
+                            const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
+                            int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!q || !meta || !block_table || !seq_lens || !schedule || !out_k || !out_idx)
+        return SPARROW_EINVAL;
+    if (k_max < 1 || schedule->bin_tokens < 1 || schedule->n_bins < 1 || schedule->frac_den < 1 ||
+        !schedule->min_pages || !schedule->frac_num)
+        return SPARROW_EINVAL;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    if ((int64_t)shape->batch * shape->num_kv_heads > 65535)
+        return SPARROW_EINVAL;
+    if (!workspace || ws_bytes < score_topk_workspace(*shape))
+        return SPARROW_EWORKSPACE;
+    Sched sched{schedule->bin_tokens, schedule->n_bins, schedule->frac_den, schedule->min_pages,
+                schedule->frac_num};
+    return status_of(launch_score_topk(*shape, q, meta, block_table, seq_lens, sched, k_max,
+                                       out_k, out_idx, workspace,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, const void *k_cache,
+                               const void *v_cache, const int32_t *block_table,
+                               const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
+                               int32_t k_max, float scale, void *out, int32_t out_dtype,
+                               void *workspace, size_t ws_bytes, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !k || !idx || !out)
+        return SPARROW_EINVAL;
+    if (k_max < 1)
+        return SPARROW_EINVAL;
+    if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
+        return SPARROW_EUNSUPPORTED;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    const AttnPlan plan = plan_attention(*shape, k_max);
+    if (plan.max_splits > 65535 || (int64_t)shape->batch * shape->num_kv_heads > 65535)
+        return SPARROW_EINVAL;
+    if (!workspace || ws_bytes < plan.workspace_bytes)
+        return SPARROW_EWORKSPACE;
+    return status_of(launch_attention(*shape, plan, q, k_cache, v_cache, block_table, seq_lens, k,
+                                      idx, k_max, scale, out, out_dtype, workspace,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const void *k_cache,
+                              const void *v_cache, const int32_t *block_table,
+                              const int32_t *seq_lens, float scale, void *out, int32_t out_dtype,
+                              void *workspace, size_t ws_bytes, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+        return SPARROW_EINVAL;
+    if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
+        return SPARROW_EUNSUPPORTED;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    const AttnPlan plan = plan_attention(*shape, shape->max_pages_per_seq);
+    if (plan.max_splits > 65535 || (int64_t)shape->batch * shape->num_kv_heads > 65535)
+        return SPARROW_EINVAL;
+    if (!workspace || ws_bytes < plan.workspace_bytes)
+        return SPARROW_EWORKSPACE;
+    return status_of(launch_attention(*shape, plan, q, k_cache, v_cache, block_table, seq_lens,
+                                      nullptr, nullptr, 0, scale, out, out_dtype, workspace,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32_t op)
+{
+    if (check_shape(shape) != SPARROW_OK)
+        return 0;
+    switch (op) {
+    case SPARROW_OP_SCORE_TOPK: return score_topk_workspace(*shape);
+    case SPARROW_OP_SPARSE_ATTN: return k_max < 1 ? 0 : plan_attention(*shape, k_max).workspace_bytes;
+    case SPARROW_OP_DENSE_ATTN:
+        return plan_attention(*shape, shape->max_pages_per_seq).workspace_bytes;
+    default: return 0;
+    }
+}
+
+const char *sparrow_status_string(int32_t status)
+{
+    switch (status) {
+    case SPARROW_OK: return "ok";
+    case SPARROW_EINVAL: return "invalid argument (null pointer or bad size)";
+    case SPARROW_EUNSUPPORTED: return "unsupported head_dim, page size, group size or dtype";
+    case SPARROW_EWORKSPACE: return "workspace missing or too small";
+    case SPARROW_EHIP: return "kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

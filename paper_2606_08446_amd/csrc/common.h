@@ -1,0 +1,109 @@
+// Internal helpers shared by the gfx950 kernels of libsparrow (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "sparrow.h"
+
+namespace sparrow {
+
+constexpr int kHeadDim = 128;
+
+// MFMA operand / accumulator types (wave64, 16x16 tiles).
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));  // 16x16x32 bf16 operand
+typedef short s16x4_t __attribute__((ext_vector_type(4)));     // 16x16x16 bf16 operand
+typedef float f32x4_t __attribute__((ext_vector_type(4)));     // 16x16 fp32 accumulator
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Budget schedule as the kernels see it (tables are device pointers).
+struct Sched {
+    int32_t bin_tokens;
+    int32_t n_bins;
+    int32_t frac_den;
+    const int32_t *min_pages;
+    const int32_t *frac_num;
+};
+
+__device__ __forceinline__ u32x4_t ld16(const void *p)
+{
+    return *reinterpret_cast<const u32x4_t *>(p);
+}
+
+__device__ __forceinline__ void st16(void *p, u32x4_t v)
+{
+    *reinterpret_cast<u32x4_t *>(p) = v;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Two fp32 values -> packed bf16 pair (round to nearest even), lo in bits 0..15.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    bf16x2_t v = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){lo, hi},
+                                         bf16x2_t);
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// One fp32 value -> bf16 bits (round to nearest even).
+__device__ __forceinline__ uint32_t to_bf16_bits(float x) { return pack_bf16(x, 0.f) & 0xffffu; }
+
+// Sequence length clamped to what the block table can address.
+__device__ __forceinline__ int clamp_len(int L, int ps, int max_pages)
+{
+    const int cap = ps * max_pages;
+    return L < 0 ? 0 : (L > cap ? cap : L);
+}
+
+// Page budget of a sequence of L tokens from the schedule, capped at k_max.
+__device__ __forceinline__ int budget_pages(int L, int ps, const Sched &s, int k_max)
+{
+    if (L <= 0)
+        return 0;
+    const int64_t n = (L + ps - 1) / ps;
+    int bin = (L - 1) / s.bin_tokens;
+    if (bin > s.n_bins - 1)
+        bin = s.n_bins - 1;
+    int64_t k = (n * (int64_t)s.frac_num[bin] + s.frac_den - 1) / s.frac_den;
+    const int64_t floor_pages = s.min_pages[bin];
+    if (k < floor_pages)
+        k = floor_pages;
+    if (k < 1)
+        k = 1;
+    if (k > n)
+        k = n;
+    if (k > k_max)
+        k = k_max;
+    return (int)k;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Launchers (host side, one per kernel family).  All return hipSuccess or the launch error.
+// ---------------------------------------------------------------------------------------------
+hipError_t launch_meta_update(const sparrow_shape_t &s, const void *k_cache,
+                              const int32_t *block_table, const int32_t *seq_lens,
+                              const int32_t *first_pos, void *meta, hipStream_t stream);
+
+size_t score_topk_workspace(const sparrow_shape_t &s);
+hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void *meta,
+                             const int32_t *block_table, const int32_t *seq_lens,
+                             const Sched &sched, int32_t k_max, int32_t *out_k,
+                             int32_t *out_idx, void *workspace, hipStream_t stream);
+
+struct AttnPlan {
+    int pages_per_split;
+    int max_splits;
+    size_t workspace_bytes;
+};
+AttnPlan plan_attention(const sparrow_shape_t &s, int32_t max_count);
+hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
+                            const void *k_cache, const void *v_cache, const int32_t *block_table,
+                            const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
+                            int32_t k_max, float scale, void *out, int out_dtype,
+                            void *workspace, hipStream_t stream);
+
+}  // namespace sparrow

@@ -1,0 +1,317 @@
+"""Python binding of libsparrow (the C ABI declared in include/sparrow.h).
+
+Argument marshalling only: every step of the sparse-decode path runs in the
+library's HIP kernels.  PyTorch provides device memory and the stream.  The
+functions named ``sparrow_*`` mirror the C entry points one to one (raw
+pointers); the functions without the prefix take torch tensors, allocate the
+workspace when none is given, and raise ``SparrowError`` on a negative status.
+
+There is no fallback: if ``libsparrow.so`` has not been built, or no GPU is
+visible, the tensor-level calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsparrow.so")
+
+SPARROW_OK = 0
+SPARROW_EINVAL = -1
+SPARROW_EUNSUPPORTED = -2
+SPARROW_EWORKSPACE = -3
+SPARROW_EHIP = -4
+SPARROW_MAX_PAGES_PER_SEQ = 15360
+SPARROW_OUT_F32 = 0
+SPARROW_OUT_BF16 = 1
+SPARROW_OP_SCORE_TOPK = 0
+SPARROW_OP_SPARSE_ATTN = 1
+SPARROW_OP_DENSE_ATTN = 2
+
+EXPORTS = ("sparrow_page_meta_update", "sparrow_page_score_topk", "sparrow_sparse_decode_attn",
+           "sparrow_dense_decode_attn", "sparrow_workspace_size", "sparrow_status_string")
+
+
+class SparrowError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {status} ({status_string(status)})")
+        self.status = status
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+                ("num_phys_pages", ctypes.c_int64)]
+
+
+class Schedule(ctypes.Structure):
+    _fields_ = [("bin_tokens", ctypes.c_int32), ("n_bins", ctypes.c_int32),
+                ("min_pages", ctypes.c_void_p), ("frac_num", ctypes.c_void_p),
+                ("frac_den", ctypes.c_int32)]
+
+
+_lib = None
+_p = ctypes.c_void_p
+_i32 = ctypes.c_int32
+
+
+def load():
+    """Load libsparrow.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2606_08446_amd.build` (no fallback exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    sp = ctypes.POINTER(Shape)
+    lib.sparrow_page_meta_update.argtypes = [sp, _p, _p, _p, _p, _p, _p]
+    lib.sparrow_page_score_topk.argtypes = [sp, _p, _p, _p, _p, ctypes.POINTER(Schedule), _i32,
+                                            _p, _p, _p, ctypes.c_size_t, _p]
+    lib.sparrow_sparse_decode_attn.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _i32,
+                                               ctypes.c_float, _p, _i32, _p, ctypes.c_size_t, _p]
+    lib.sparrow_dense_decode_attn.argtypes = [sp, _p, _p, _p, _p, _p, ctypes.c_float, _p, _i32,
+                                              _p, ctypes.c_size_t, _p]
+    for fn in EXPORTS[:4]:
+        getattr(lib, fn).restype = ctypes.c_int
+    lib.sparrow_workspace_size.argtypes = [sp, _i32, _i32]
+    lib.sparrow_workspace_size.restype = ctypes.c_size_t
+    lib.sparrow_status_string.argtypes = [_i32]
+    lib.sparrow_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------------ raw entry points (C names)
+def sparrow_page_meta_update(shape, k_cache, block_table, seq_lens, first_pos, meta, stream):
+    return load().sparrow_page_meta_update(ctypes.byref(shape), k_cache, block_table, seq_lens,
+                                           first_pos, meta, stream)
+
+
+def sparrow_page_score_topk(shape, q, meta, block_table, seq_lens, schedule, k_max, out_k,
+                            out_idx, workspace, ws_bytes, stream):
+    return load().sparrow_page_score_topk(ctypes.byref(shape), q, meta, block_table, seq_lens,
+                                          ctypes.byref(schedule), k_max, out_k, out_idx,
+                                          workspace, ws_bytes, stream)
+
+
+def sparrow_sparse_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens, k, idx, k_max,
+                               scale, out, out_dtype, workspace, ws_bytes, stream):
+    return load().sparrow_sparse_decode_attn(ctypes.byref(shape), q, k_cache, v_cache,
+                                             block_table, seq_lens, k, idx, k_max, scale, out,
+                                             out_dtype, workspace, ws_bytes, stream)
+
+
+def sparrow_dense_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens, scale, out,
+                              out_dtype, workspace, ws_bytes, stream):
+    return load().sparrow_dense_decode_attn(ctypes.byref(shape), q, k_cache, v_cache,
+                                            block_table, seq_lens, scale, out, out_dtype,
+                                            workspace, ws_bytes, stream)
+
+
+def sparrow_workspace_size(shape, k_max, op) -> int:
+    return int(load().sparrow_workspace_size(ctypes.byref(shape), k_max, op))
+
+
+def sparrow_status_string(status) -> str:
+    return load().sparrow_status_string(status).decode()
+
+
+status_string = sparrow_status_string
+
+
+# ------------------------------------------------------------------ host helpers
+def make_shape(batch, num_q_heads, num_kv_heads, page_size, max_pages_per_seq, num_phys_pages,
+               head_dim=128) -> Shape:
+    return Shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq,
+                 num_phys_pages)
+
+
+def shape_of(q, k_cache, block_table) -> Shape:
+    """Shape struct from tensors q [B][Hq][D], k_cache [P][Hkv][ps][D], block_table [B][M]."""
+    B, Hq, D = q.shape
+    P, Hkv, ps, _ = k_cache.shape
+    return make_shape(B, Hq, Hkv, ps, block_table.shape[1], P, head_dim=D)
+
+
+def budget_bound(seq_lens: Sequence[int], page_size: int, bin_tokens: int,
+                 min_pages: Sequence[int], frac_num: Sequence[int], frac_den: int) -> int:
+    """Largest schedule budget over host-known lengths, to size ``k_max`` (at least 1)."""
+    best = 1
+    nb = len(min_pages)
+    for L in seq_lens:
+        L = int(L)
+        if L <= 0:
+            continue
+        n = -(-L // page_size)
+        b = min((L - 1) // bin_tokens, nb - 1)
+        k = max(int(min_pages[b]), -(-(n * int(frac_num[b])) // frac_den))
+        best = max(best, min(max(k, 1), n))
+    return best
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device=None) -> int:
+    import torch
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check(fn: str, rc: int) -> None:
+    if rc != SPARROW_OK:
+        raise SparrowError(fn, rc)
+
+
+def _workspace(nbytes: int, device):
+    import torch
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+
+
+def _require_device(t):
+    if not t.is_cuda:
+        raise RuntimeError("libsparrow runs on the GPU only: tensors must be on a HIP device")
+
+
+# ------------------------------------------------------------------ tensor-level wrappers
+def page_meta_update(k_cache, block_table, seq_lens, meta, first_pos=None, shape=None):
+    """Rebuild (first_pos None) or update the min/max metadata in ``meta`` (in place)."""
+    _require_device(k_cache)
+    if shape is None:
+        P, Hkv, ps, D = k_cache.shape
+        shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D)
+    rc = sparrow_page_meta_update(shape, _ptr(k_cache), _ptr(block_table), _ptr(seq_lens),
+                                  _ptr(first_pos), _ptr(meta), _stream(k_cache.device))
+    _check("sparrow_page_meta_update", rc)
+    return meta
+
+
+def page_score_topk(q, meta, block_table, seq_lens, k_cache_shape, min_pages, frac_num,
+                    frac_den, bin_tokens, k_max, out_k=None, out_idx=None, workspace=None):
+    """Scores, budgets and top-k page lists.  Returns (k [B] int32, idx [B][Hkv][k_max] int32)."""
+    import torch
+    _require_device(q)
+    P, Hkv, ps, D = k_cache_shape
+    shape = make_shape(q.shape[0], q.shape[1], Hkv, ps, block_table.shape[1], P, D)
+    sched = Schedule(int(bin_tokens), int(min_pages.numel()), _ptr(min_pages), _ptr(frac_num),
+                     int(frac_den))
+    dev = q.device
+    if out_k is None:
+        out_k = torch.empty(q.shape[0], dtype=torch.int32, device=dev)
+    if out_idx is None:
+        out_idx = torch.empty((q.shape[0], Hkv, int(k_max)), dtype=torch.int32, device=dev)
+    need = sparrow_workspace_size(shape, int(k_max), SPARROW_OP_SCORE_TOPK)
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    rc = sparrow_page_score_topk(shape, _ptr(q), _ptr(meta), _ptr(block_table), _ptr(seq_lens),
+                                 sched, int(k_max), _ptr(out_k), _ptr(out_idx), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(dev))
+    _check("sparrow_page_score_topk", rc)
+    return out_k, out_idx
+
+
+def sparse_decode_attn(q, k_cache, v_cache, block_table, seq_lens, k, idx, scale=None, out=None,
+                       out_dtype=SPARROW_OUT_F32, workspace=None):
+    """Attention over the selected pages.  Returns out [B][Hq][D] (fp32 or bf16)."""
+    import torch
+    _require_device(q)
+    shape = shape_of(q, k_cache, block_table)
+    k_max = int(idx.shape[2])
+    scale = 1.0 / math.sqrt(q.shape[2]) if scale is None else scale
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32 if out_dtype == SPARROW_OUT_F32
+                          else torch.bfloat16, device=q.device)
+    need = sparrow_workspace_size(shape, k_max, SPARROW_OP_SPARSE_ATTN)
+    if workspace is None:
+        workspace = _workspace(need, q.device)
+    rc = sparrow_sparse_decode_attn(shape, _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                    _ptr(block_table), _ptr(seq_lens), _ptr(k), _ptr(idx), k_max,
+                                    float(scale), _ptr(out), int(out_dtype), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(),
+                                    _stream(q.device))
+    _check("sparrow_sparse_decode_attn", rc)
+    return out
+
+
+def dense_decode_attn(q, k_cache, v_cache, block_table, seq_lens, scale=None, out=None,
+                      out_dtype=SPARROW_OUT_F32, workspace=None):
+    """Dense paged decode attention.  Returns out [B][Hq][D] (fp32 or bf16)."""
+    import torch
+    _require_device(q)
+    shape = shape_of(q, k_cache, block_table)
+    scale = 1.0 / math.sqrt(q.shape[2]) if scale is None else scale
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32 if out_dtype == SPARROW_OUT_F32
+                          else torch.bfloat16, device=q.device)
+    need = sparrow_workspace_size(shape, 0, SPARROW_OP_DENSE_ATTN)
+    if workspace is None:
+        workspace = _workspace(need, q.device)
+    rc = sparrow_dense_decode_attn(shape, _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                   _ptr(block_table), _ptr(seq_lens), float(scale), _ptr(out),
+                                   int(out_dtype), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(),
+                                   _stream(q.device))
+    _check("sparrow_dense_decode_attn", rc)
+    return out
+
+
+class SparseDecodeStep:
+    """One layer's sparse decode step with preallocated buffers.
+
+    ``run(first_pos)`` enqueues: metadata update of the pages touched since
+    ``first_pos`` (skipped when None), page scoring + top-k, sparse attention."""
+
+    def __init__(self, q, k_cache, v_cache, block_table, seq_lens, meta, min_pages, frac_num,
+                 frac_den, bin_tokens, k_max, scale=None):
+        import torch
+        _require_device(q)
+        self.q, self.k_cache, self.v_cache = q, k_cache, v_cache
+        self.block_table, self.seq_lens, self.meta = block_table, seq_lens, meta
+        self.shape = shape_of(q, k_cache, block_table)
+        self.sched = Schedule(int(bin_tokens), int(min_pages.numel()), _ptr(min_pages),
+                              _ptr(frac_num), int(frac_den))
+        self._tables = (min_pages, frac_num)
+        self.k_max = int(k_max)
+        self.scale = 1.0 / math.sqrt(q.shape[2]) if scale is None else float(scale)
+        dev = q.device
+        B, Hkv = q.shape[0], k_cache.shape[1]
+        self.k = torch.empty(B, dtype=torch.int32, device=dev)
+        self.idx = torch.empty((B, Hkv, self.k_max), dtype=torch.int32, device=dev)
+        self.out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+        self.ws_score = _workspace(sparrow_workspace_size(self.shape, self.k_max,
+                                                          SPARROW_OP_SCORE_TOPK), dev)
+        self.ws_attn = _workspace(sparrow_workspace_size(self.shape, self.k_max,
+                                                         SPARROW_OP_SPARSE_ATTN), dev)
+
+    def meta_update(self, first_pos, stream):
+        _check("sparrow_page_meta_update", sparrow_page_meta_update(
+            self.shape, _ptr(self.k_cache), _ptr(self.block_table), _ptr(self.seq_lens),
+            _ptr(first_pos), _ptr(self.meta), stream))
+
+    def score_topk(self, stream):
+        _check("sparrow_page_score_topk", sparrow_page_score_topk(
+            self.shape, _ptr(self.q), _ptr(self.meta), _ptr(self.block_table),
+            _ptr(self.seq_lens), self.sched, self.k_max, _ptr(self.k), _ptr(self.idx),
+            _ptr(self.ws_score), self.ws_score.numel(), stream))
+
+    def attend(self, stream):
+        _check("sparrow_sparse_decode_attn", sparrow_sparse_decode_attn(
+            self.shape, _ptr(self.q), _ptr(self.k_cache), _ptr(self.v_cache),
+            _ptr(self.block_table), _ptr(self.seq_lens), _ptr(self.k), _ptr(self.idx),
+            self.k_max, self.scale, _ptr(self.out), SPARROW_OUT_F32, _ptr(self.ws_attn),
+            self.ws_attn.numel(), stream))
+
+    def run(self, first_pos=None, stream=None):
+        stream = _stream(self.q.device) if stream is None else stream
+        if first_pos is not None:
+            self.meta_update(first_pos, stream)
+        self.score_topk(stream)
+        self.attend(stream)
+        return self.out

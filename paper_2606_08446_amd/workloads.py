@@ -274,3 +274,12 @@ def small(B=2, Hq=4, Hkv=2, ps=16, lengths=(40, 70), seed=0, schedule=None, **kw
 def bf16_bits(t: torch.Tensor) -> np.ndarray:
     """bf16 tensor -> numpy uint16 bit patterns (on the host)."""
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def with_schedule(inp: Inputs, w: Workload) -> Inputs:
+    """The same caches and queries under workload ``w``'s budget schedule."""
+    dev = inp.q.device
+    return dataclasses.replace(
+        inp, workload=w,
+        min_pages=torch.as_tensor(np.array(w.schedule.min_pages, np.int32), device=dev),
+        frac_num=torch.as_tensor(np.array(w.schedule.frac_num, np.int32), device=dev))

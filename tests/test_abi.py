@@ -1,0 +1,190 @@
+"""The C-ABI library: it loads, exports what include/sparrow.h declares, and
+rejects bad host-visible arguments with the documented status before any GPU
+work is enqueued.  Runs on the CPU (no compute call reaches a kernel)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_08446_amd import sparrow as S
+from paper_2606_08446_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparrow.h")
+FAKE = 0x1000  # non-null address that no test call ever dereferences
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^[A-Za-z_][\w \*]*?\b(sparrow_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(S.LIB_PATH):
+        from paper_2606_08446_amd import build
+        build.build_library()
+    return S.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(S.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    consts = dict(re.findall(r"#define (SPARROW_\w+) \(?(-?\d+)\)?", text))
+    for name, value in consts.items():
+        assert getattr(S, name) == int(value), name
+
+
+def good_shape(**kw):
+    d = dict(batch=4, num_q_heads=16, num_kv_heads=8, page_size=16, max_pages_per_seq=64,
+             num_phys_pages=300)
+    d.update(kw)
+    return S.make_shape(**d)
+
+
+BAD_SHAPES = [
+    (dict(head_dim=64), S.SPARROW_EUNSUPPORTED),
+    (dict(num_q_heads=12, num_kv_heads=8), S.SPARROW_EINVAL),
+    (dict(page_size=8), S.SPARROW_EUNSUPPORTED),
+    (dict(page_size=48), S.SPARROW_EUNSUPPORTED),
+    (dict(num_q_heads=136, num_kv_heads=8), S.SPARROW_EUNSUPPORTED),   # G = 17
+    (dict(max_pages_per_seq=S.SPARROW_MAX_PAGES_PER_SEQ + 1), S.SPARROW_EUNSUPPORTED),
+    (dict(max_pages_per_seq=0), S.SPARROW_EINVAL),
+    (dict(batch=-1), S.SPARROW_EINVAL),
+    (dict(num_kv_heads=0), S.SPARROW_EINVAL),
+    (dict(num_phys_pages=0), S.SPARROW_EINVAL),
+]
+
+
+def sched():
+    return S.Schedule(2048, 1, FAKE, FAKE, 10)
+
+
+def call(fn, shape, **over):
+    """Call entry point `fn` with plausible fake pointers, overriding some arguments."""
+    ws = over.pop("ws", FAKE)
+    ws_bytes = over.pop("ws_bytes", 1 << 40)
+    if fn == "meta":
+        a = dict(k_cache=FAKE, bt=FAKE, lens=FAKE, first_pos=FAKE, meta=FAKE)
+        a.update(over)
+        return S.sparrow_page_meta_update(shape, a["k_cache"], a["bt"], a["lens"], a["first_pos"],
+                                          a["meta"], None)
+    if fn == "topk":
+        a = dict(q=FAKE, meta=FAKE, bt=FAKE, lens=FAKE, sched=sched(), k_max=8, out_k=FAKE,
+                 out_idx=FAKE)
+        a.update(over)
+        return S.sparrow_page_score_topk(shape, a["q"], a["meta"], a["bt"], a["lens"], a["sched"],
+                                         a["k_max"], a["out_k"], a["out_idx"], ws, ws_bytes, None)
+    if fn == "sparse":
+        a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, kk=FAKE, idx=FAKE, k_max=8,
+                 out=FAKE, dtype=0)
+        a.update(over)
+        return S.sparrow_sparse_decode_attn(shape, a["q"], a["k"], a["v"], a["bt"], a["lens"],
+                                            a["kk"], a["idx"], a["k_max"], 0.088, a["out"],
+                                            a["dtype"], ws, ws_bytes, None)
+    a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, dtype=0)
+    a.update(over)
+    return S.sparrow_dense_decode_attn(shape, a["q"], a["k"], a["v"], a["bt"], a["lens"], 0.088,
+                                       a["out"], a["dtype"], ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("fn", ["meta", "topk", "sparse", "dense"])
+@pytest.mark.parametrize("bad,status", BAD_SHAPES)
+def test_bad_shapes_are_rejected(lib, fn, bad, status):
+    bad = dict(bad)
+    head_dim = bad.pop("head_dim", 128)
+    shape = good_shape(**bad)
+    shape.head_dim = head_dim
+    assert call(fn, shape) == status
+
+
+NULLS = {
+    "meta": ["k_cache", "bt", "lens", "meta"],
+    "topk": ["q", "meta", "bt", "lens", "out_k", "out_idx"],
+    "sparse": ["q", "k", "v", "bt", "lens", "kk", "idx", "out"],
+    "dense": ["q", "k", "v", "bt", "lens", "out"],
+}
+
+
+@pytest.mark.parametrize("fn,arg", [(f, a) for f, args in NULLS.items() for a in args])
+def test_null_pointers_are_rejected(lib, fn, arg):
+    assert call(fn, good_shape(), **{arg: None}) == S.SPARROW_EINVAL
+
+
+def test_null_shape_and_schedule_are_rejected(lib):
+    assert lib.sparrow_page_meta_update(None, FAKE, FAKE, FAKE, None, FAKE, None) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), sched=S.Schedule(0, 1, FAKE, FAKE, 10)) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), sched=S.Schedule(2048, 0, FAKE, FAKE, 10)) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), sched=S.Schedule(2048, 1, FAKE, FAKE, 0)) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), sched=S.Schedule(2048, 1, None, FAKE, 10)) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    assert call("sparse", good_shape(), k_max=0) == S.SPARROW_EINVAL
+
+
+def test_unsupported_output_dtype(lib):
+    assert call("sparse", good_shape(), dtype=2) == S.SPARROW_EUNSUPPORTED
+    assert call("dense", good_shape(), dtype=7) == S.SPARROW_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("fn,op", [("topk", S.SPARROW_OP_SCORE_TOPK),
+                                   ("sparse", S.SPARROW_OP_SPARSE_ATTN),
+                                   ("dense", S.SPARROW_OP_DENSE_ATTN)])
+def test_workspace_checks(lib, fn, op):
+    shape = good_shape()
+    need = S.sparrow_workspace_size(shape, 8, op)
+    assert need > 0
+    assert call(fn, shape, ws=None) == S.SPARROW_EWORKSPACE
+    assert call(fn, shape, ws_bytes=need - 1) == S.SPARROW_EWORKSPACE
+
+
+def test_empty_batch_enqueues_nothing(lib):
+    shape = good_shape(batch=0)
+    for fn in ("meta", "topk", "sparse", "dense"):
+        assert call(fn, shape, ws=None, ws_bytes=0) == S.SPARROW_OK
+
+
+def test_workspace_size_properties(lib):
+    shape = good_shape()
+    assert S.sparrow_workspace_size(shape, 8, 99) == 0
+    assert S.sparrow_workspace_size(good_shape(page_size=8), 8, 0) == 0
+    assert S.sparrow_workspace_size(shape, 0, S.SPARROW_OP_SPARSE_ATTN) == 0
+    a = S.sparrow_workspace_size(shape, 8, S.SPARROW_OP_SPARSE_ATTN)
+    b = S.sparrow_workspace_size(shape, 64, S.SPARROW_OP_SPARSE_ATTN)
+    assert 0 < a <= b
+    assert S.sparrow_workspace_size(shape, 1, S.SPARROW_OP_SCORE_TOPK) == 4 * 8 * 64 * 4
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -99):
+        assert isinstance(S.sparrow_status_string(code), str)
+    assert S.sparrow_status_string(-3) != S.sparrow_status_string(-1)
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c5"])
+def test_host_budget_bound_matches_oracle(cfg):
+    w = W.CONFIGS[cfg]
+    s = w.schedule
+    rng = np.random.default_rng(3)
+    lens = rng.integers(w.len_lo, w.len_hi + 1, size=200)
+    want = int(oracle.budgets(lens, w.page_size, s.bin_tokens, s.min_pages, s.frac_num,
+                              s.frac_den).max())
+    assert S.budget_bound(lens, w.page_size, s.bin_tokens, s.min_pages, s.frac_num,
+                          s.frac_den) == want
+
+
+def test_tensor_wrappers_refuse_host_tensors():
+    import torch
+    q = torch.zeros(1, 2, 128, dtype=torch.bfloat16)
+    with pytest.raises(RuntimeError):
+        S.dense_decode_attn(q, torch.zeros(2, 1, 16, 128, dtype=torch.bfloat16),
+                            torch.zeros(2, 1, 16, 128, dtype=torch.bfloat16),
+                            torch.zeros(1, 2, dtype=torch.int32), torch.ones(1, dtype=torch.int32))

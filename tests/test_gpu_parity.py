@@ -1,0 +1,316 @@
+"""GPU parity: the HIP path (called through the C ABI) against the CPU oracle.
+
+Small cases are checked in full (every sequence, head, page and output
+element), at sizes that span several tiles of every kernel plus ragged tails.
+The five workload shapes run at full size on the GPU and are checked on a
+seeded sample of sequences.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_08446_amd import sparrow as S
+from paper_2606_08446_amd import workloads as W
+
+from parity import (SCALE, check_indices, check_meta, check_out, full_check, gpu_run, host, log,
+                    sample_inputs)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu(gpu_device):
+    S.load()
+    yield
+
+
+def small_inputs(G, Hkv, ps, lengths, seed, schedule, **kw):
+    w = W.small(B=len(lengths), Hq=G * Hkv, Hkv=Hkv, ps=ps, lengths=lengths, seed=seed,
+                schedule=schedule, **kw)
+    return W.generate(w, DEV, lengths=list(lengths))
+
+
+# ---------------------------------------------------------------------------------- C1 in full
+def test_c1_full():
+    log("case c1 full")
+    inp = W.generate(W.C1, DEV)
+    r = full_check(inp)
+    assert r["gpu"]["k"].tolist() == [32]
+    # the x4 sink page carries the largest keys; it must be selected for every head
+    assert (r["gpu"]["idx"][0, :, 0] == 0).all()
+
+
+# ---------------------------------------------------------------------------------- small sweep
+SWEEP = [
+    # (G, Hkv, ps, lengths, schedule)
+    (2, 2, 16, (1, 16, 17, 300, 4100), W.fraction_budget(1, 3)),
+    (1, 3, 16, (33, 5000, 2, 15), W.fraction_budget(1, 10)),
+    (4, 2, 16, (9000, 4097, 4096), W.fraction_budget(5, 100, floor_pages=3)),
+    (5, 2, 16, (777, 6000, 31), W.rising_permille(2048, 2048, 8192, 30, 150)),
+    (8, 1, 16, (2500, 64, 65), W.fixed_budget(7)),
+    (16, 1, 16, (1000, 3333), W.fraction_budget(1, 4)),
+    (2, 2, 32, (1, 32, 33, 8000, 20000), W.fraction_budget(1, 8)),
+    (4, 2, 64, (64, 65, 9000), W.fraction_budget(1, 5)),
+    (2, 2, 128, (127, 128, 129, 30000), W.fraction_budget(1, 6)),
+    (3, 2, 16, (0, 50, 0, 1200), W.fraction_budget(1, 2)),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SWEEP)))
+def test_small_sweep(case):
+    G, Hkv, ps, lengths, sched = SWEEP[case]
+    log(f"case sweep {case}: G={G} Hkv={Hkv} ps={ps} lens={lengths}")
+    inp = small_inputs(G, Hkv, ps, lengths, seed=100 + case, schedule=sched)
+    full_check(inp)
+
+
+@pytest.mark.parametrize("k_pages", ["one", "n_minus_1", "n", "more"])
+def test_budget_edges(k_pages):
+    lengths = (800, 801, 3000)
+    n = [(L + 15) // 16 for L in lengths]
+    fixed = {"one": 1, "n_minus_1": min(n) - 1, "n": max(n), "more": max(n) + 50}[k_pages]
+    log(f"case budget edge {k_pages}: fixed={fixed}")
+    inp = small_inputs(4, 2, 16, lengths, seed=7, schedule=W.fixed_budget(fixed))
+    r = full_check(inp)
+    if k_pages in ("n", "more"):
+        for b, nb in enumerate(n):
+            assert r["gpu"]["k"][b] == nb
+
+
+def test_k_max_caps_the_budget():
+    log("case k_max cap")
+    inp = small_inputs(2, 2, 16, (3000, 5000), seed=8, schedule=W.fraction_budget(1, 2))
+    r = full_check(inp, k_max=40)
+    assert (r["gpu"]["k"] == 40).all()
+
+
+def test_bf16_output():
+    log("case bf16 output")
+    inp = small_inputs(4, 2, 16, (700, 2900), seed=9, schedule=W.fraction_budget(1, 5))
+    full_check(inp, out_dtype=S.SPARROW_OUT_BF16)
+
+
+# ---------------------------------------------------------------------------------- ties
+def test_zero_query_selects_lowest_pages():
+    log("case zero query")
+    inp = small_inputs(4, 2, 16, (2000, 5000), seed=10, schedule=W.fixed_budget(9))
+    inp.q.zero_()
+    r = full_check(inp)
+    for b in range(2):
+        for h in range(2):
+            assert r["gpu"]["idx"][b, h, :9].tolist() == list(range(9))
+
+
+def test_duplicated_pages_keep_lower_index():
+    log("case duplicated pages")
+    inp = small_inputs(2, 2, 16, (4000,), seed=11, schedule=W.fixed_budget(5))
+    bt = inp.block_table.cpu().numpy()
+    # pages 3, 40, 200 and 201 all get copies of page 100's keys, boosted to be on top
+    src = int(bt[0, 100])
+    inp.k_cache[src] = (inp.k_cache[src].float() * 3).to(torch.bfloat16)
+    for p in (3, 40, 200, 201):
+        inp.k_cache[int(bt[0, p])] = inp.k_cache[src]
+    r = full_check(inp)
+    for h in range(2):
+        sel = r["gpu"]["idx"][0, h, :5].tolist()
+        assert sel == [3, 40, 100, 200, 201]
+
+
+def test_duplicated_pages_at_the_cut():
+    log("case duplicated pages at the cut")
+    inp = small_inputs(2, 1, 16, (3000,), seed=12, schedule=W.fixed_budget(2))
+    bt = inp.block_table.cpu().numpy()
+    src = int(bt[0, 50])
+    inp.k_cache[src] = (inp.k_cache[src].float() * 3).to(torch.bfloat16)
+    for p in (10, 150):
+        inp.k_cache[int(bt[0, p])] = inp.k_cache[src]
+    # three identical top pages, budget 2: the two lowest indices win
+    r = full_check(inp)
+    assert r["gpu"]["idx"][0, 0, :2].tolist() == [10, 50]
+
+
+def test_signed_zero_keys_and_scores():
+    log("case signed zeros")
+    inp = small_inputs(2, 2, 16, (900, 333), seed=13, schedule=W.fixed_budget(6))
+    k = inp.k_cache
+    # whole pages of +0 / -0 keys: their scores are zero of either sign and tie
+    bt = inp.block_table.cpu().numpy()
+    for p, sign in ((5, 1.0), (6, -1.0), (7, 1.0)):
+        k[int(bt[0, p])] = torch.zeros_like(k[int(bt[0, p])]) * sign
+    half = k[int(bt[1, 2])].view(torch.int16)
+    half[:, :, 0::2] = 0
+    half[:, :, 1::2] = -32768  # bf16 -0
+    full_check(inp)
+
+
+# ---------------------------------------------------------------------------------- metadata
+@pytest.mark.parametrize("step", [1, 9, 40])
+def test_meta_incremental_update_equals_rebuild(step):
+    log(f"case meta update step {step}")
+    inp = small_inputs(2, 4, 16, (100, 2000, 17, 5), seed=14, schedule=W.fixed_budget(3))
+    full = inp.seq_lens.clone()
+    short = torch.clamp(full - step, min=0)
+    meta = torch.zeros((inp.num_phys_pages, 4, 2, 128), dtype=torch.bfloat16, device=DEV)
+    S.page_meta_update(inp.k_cache, inp.block_table, short, meta)
+    S.page_meta_update(inp.k_cache, inp.block_table, full, meta, first_pos=short)
+    rebuilt = torch.zeros_like(meta)
+    S.page_meta_update(inp.k_cache, inp.block_table, full, rebuilt)
+    torch.cuda.synchronize()
+    h = host(inp)
+    pages = [int(x) for b, L in enumerate(h["lens"]) for x in h["bt"][b, :(int(L) + 15) // 16]]
+    g1, g2 = W.bf16_bits(meta), W.bf16_bits(rebuilt)
+    np.testing.assert_array_equal(g1[pages], g2[pages])
+    check_meta(g1, oracle.page_meta(h["k"], h["bt"], h["lens"]), h["bt"], h["lens"], 16)
+
+
+@pytest.mark.parametrize("ps", [32, 64, 128])
+def test_meta_update_larger_pages(ps):
+    log(f"case meta update ps {ps}")
+    inp = small_inputs(2, 2, ps, (ps * 3 + 5, ps - 1), seed=15, schedule=W.fixed_budget(2))
+    meta = torch.zeros((inp.num_phys_pages, 2, 2, 128), dtype=torch.bfloat16, device=DEV)
+    short = torch.clamp(inp.seq_lens - 7, min=0)
+    S.page_meta_update(inp.k_cache, inp.block_table, short, meta)
+    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta, first_pos=short)
+    torch.cuda.synchronize()
+    h = host(inp)
+    check_meta(W.bf16_bits(meta), oracle.page_meta(h["k"], h["bt"], h["lens"]), h["bt"],
+               h["lens"], ps)
+
+
+# ---------------------------------------------------------------------------------- invariants
+def test_full_budget_sparse_equals_dense_bitwise():
+    log("case full budget == dense")
+    inp = small_inputs(4, 2, 16, (3000, 777, 16), seed=16, schedule=W.fixed_budget(10000))
+    k_max = inp.max_pages  # same split plan as the dense call
+    g = gpu_run(inp, k_max)
+    np.testing.assert_array_equal(g["out_sparse"], g["out_dense"])
+
+
+def test_runs_are_deterministic():
+    log("case determinism")
+    inp = small_inputs(5, 2, 16, (6000, 2000), seed=17, schedule=W.fraction_budget(1, 7))
+    a = gpu_run(inp, 200)
+    b = gpu_run(inp, 200)
+    for key in ("meta", "k", "idx", "out_sparse", "out_dense"):
+        np.testing.assert_array_equal(a[key], b[key])
+
+
+def test_out_of_range_page_entries_are_skipped():
+    log("case invalid idx entries")
+    inp = small_inputs(2, 2, 16, (500, 900), seed=18, schedule=W.fixed_budget(4))
+    idx = torch.tensor([[[0, 3, -1, 31], [2, 40, 5, 7]],
+                        [[1, 2, 3, 4], [57, 56, 1000, 0]]], dtype=torch.int32, device=DEV)
+    k = torch.tensor([4, 4], dtype=torch.int32, device=DEV)
+    out = S.sparse_decode_attn(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+                               k, idx, SCALE)
+    torch.cuda.synchronize()
+    h = host(inp)
+    n = [(int(L) + 15) // 16 for L in h["lens"]]
+    clean = np.full((2, 2, 4), -1, np.int32)
+    kk = np.zeros(2, np.int32)
+    ref = np.zeros((2, 4, 128))
+    for b in range(2):
+        for hh in range(2):
+            valid = [p for p in idx[b, hh].tolist() if 0 <= p < n[b]]
+            sub = np.full((1, 1, 4), -1, np.int32)
+            sub[0, 0, :len(valid)] = valid
+            one = oracle.attention(h["q"][b:b + 1, 2 * hh:2 * hh + 2], h["k"][:, hh:hh + 1],
+                                   h["v"][:, hh:hh + 1], h["bt"][b:b + 1], h["lens"][b:b + 1],
+                                   SCALE, np.array([len(valid)], np.int32), sub)
+            ref[b, 2 * hh:2 * hh + 2] = one[0]
+    check_out(out.cpu().numpy().astype(np.float64), ref, "invalid-idx sparse")
+
+
+# ---------------------------------------------------------------------------------- full sizes
+def sampled_check(inp, seqs, k_max, dense=True, label=""):
+    """Full-size GPU run; oracle on the sampled sequences (all heads, all pages)."""
+    w = inp.workload
+    s = w.schedule
+    ps = w.page_size
+    log(f"  gpu run {label}: B={w.batch} P={inp.num_phys_pages} k_max={k_max}")
+    g = gpu_run(inp, k_max, dense=dense)
+    h = sample_inputs(inp, seqs)
+    log(f"  oracle on sequences {list(seqs)}")
+    ora_meta = oracle.page_meta(h["k"], h["bt"], h["lens"])
+    # compare metadata of the sampled pages (GPU meta is indexed by physical page)
+    np.testing.assert_array_equal(g["meta"][h["phys"]], ora_meta)
+    s32, s64 = oracle.page_scores(h["q"], ora_meta, h["bt"], h["lens"], ps)
+    ora_k = np.minimum(oracle.budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
+                                      s.frac_den), k_max).astype(np.int32)
+    ora_idx = oracle.select(h["lens"], ora_k, s32, ps, k_max)
+    gk = g["k"][list(seqs)]
+    gidx = g["idx"][list(seqs)]
+    excused = check_indices(gk, gidx, ora_k, ora_idx, s32, s64, h["lens"], ps, k_max)
+    log(f"  indices match ({excused} near-tie pages excused)")
+    ref_s = oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], SCALE, gk, gidx)
+    check_out(g["out_sparse"][list(seqs)], ref_s, "sparse")
+    if dense:
+        ref_d = oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], SCALE)
+        check_out(g["out_dense"][list(seqs)], ref_d, "dense")
+    return g
+
+
+def pick(inp, count, seed):
+    rng = np.random.default_rng(seed)
+    B = inp.workload.batch
+    order = np.argsort(inp.lens_host)
+    # shortest, longest and random others
+    chosen = {int(order[0]), int(order[-1])}
+    while len(chosen) < min(count, B):
+        chosen.add(int(rng.integers(0, B)))
+    return sorted(chosen)
+
+
+def bound(inp):
+    s = inp.workload.schedule
+    return S.budget_bound(inp.lens_host, inp.workload.page_size, s.bin_tokens, s.min_pages,
+                          s.frac_num, s.frac_den)
+
+
+@pytest.mark.parametrize("cfg", ["c2", "c3", "c5"])
+def test_full_size_sampled(cfg):
+    log(f"case full-size {cfg}")
+    inp = W.generate(W.CONFIGS[cfg], DEV)
+    g = sampled_check(inp, pick(inp, 4, 1), bound(inp), label=cfg)
+    if cfg == "c2":
+        # every planted hot page is kept (the budget of at least 64 pages has room)
+        for b in range(inp.workload.batch):
+            for hh in range(inp.workload.num_kv_heads):
+                assert set(inp.hot_host[b][hh]) <= set(g["idx"][b, hh].tolist())
+    del inp
+    torch.cuda.empty_cache()
+
+
+def test_full_size_c4_budget_sweep():
+    log("case full-size c4")
+    inp = W.generate(W.C4, DEV)
+    seqs = pick(inp, 3, 2)
+    for i in (0, 2, 4):
+        run = W.with_schedule(inp, W.c4_with_fraction(i))
+        sampled_check(run, seqs, bound(run), dense=(i == 4), label=run.workload.name)
+    del inp
+    torch.cuda.empty_cache()
+
+
+def test_full_size_c5_append_and_update():
+    log("case full-size c5 append")
+    w = W.C5
+    inp = W.generate(w, DEV)
+    meta = torch.zeros((inp.num_phys_pages, w.num_kv_heads, 2, 128), dtype=torch.bfloat16,
+                       device=DEV)
+    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta)
+    first = inp.seq_lens.clone()
+    inp.seq_lens += 1   # the cache already holds a token at position L (the spare page)
+    inp.lens_host = inp.lens_host + 1
+    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta, first_pos=first)
+    torch.cuda.synchronize()
+    seqs = pick(inp, 4, 3)
+    h = sample_inputs(inp, seqs)
+    np.testing.assert_array_equal(W.bf16_bits(meta)[h["phys"]],
+                                  oracle.page_meta(h["k"], h["bt"], h["lens"]))
+    sampled_check(inp, seqs, bound(inp), dense=False, label="c5 after append")
