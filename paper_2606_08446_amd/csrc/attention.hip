@@ -42,11 +42,11 @@ __device__ __forceinline__ void load_chunk(Chunk &c, const uint16_t *__restrict_
     const uint16_t *kp = kbase + lr * kHeadDim + 8 * lg;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        c.k[i] = ld16(kp + 32 * i);
+        c.k[i] = ld16_nt(kp + 32 * i);
     const uint16_t *vp = vbase + (4 * lg) * kHeadDim + 8 * lr;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-        c.v[j] = ld16(vp + j * kHeadDim);
+        c.v[j] = ld16_nt(vp + j * kHeadDim);
 }
 
 // Element `c` (0..7) of two 8 x bf16 vectors, packed as (x[c], y[c]).

@@ -33,6 +33,12 @@ __device__ __forceinline__ u32x4_t ld16(const void *p)
     return *reinterpret_cast<const u32x4_t *>(p);
 }
 
+// Streaming load (non-temporal hint) for data that is read exactly once.
+__device__ __forceinline__ u32x4_t ld16_nt(const void *p)
+{
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+}
+
 __device__ __forceinline__ void st16(void *p, u32x4_t v)
 {
     *reinterpret_cast<u32x4_t *>(p) = v;

@@ -4,15 +4,11 @@
 //     S(p) = sum_{g<G} sum_i max(q_{g,i} mn_i, q_{g,i} mx_i).
 // Because mn_i <= mx_i, max(q mn, q mx) = q+ mx + q- mn with q+ = max(q, 0) and
 // q- = min(q, 0), so S(p) = sum_i (Q-_i mn_i + Q+_i mx_i) with Q+-_i = sum_g q+-_{g,i}:
-// one 256-long dot product of the page's metadata row [mn | mx] with a weight vector w
-// that depends only on the query group.  Pages of a sequence form the rows of a
-// (pages x 256) bf16 matrix, so the scores are a matrix-vector product, run on MFMA
-// 16x16x32 bf16 tiles: 16 pages x 32 channels per instruction, w split exactly into
-// three bf16 parts (hi + mid + lo == w) placed in the first three columns of B.  The
-// three partial sums are added in fp32.  Every page goes through the same instruction
-// sequence, so pages with identical metadata get bit-identical scores (exact ties stay
-// ties).  Each workgroup scores 256 pages of one (sequence, KV head) and writes fp32
-// scores to the workspace; sequences whose budget covers every page are skipped.
+// one 256-long dot product of the page's metadata row [mn | mx] with a weight vector that
+// depends only on the query group.  This is a matrix-vector product (pages x 256 against
+// one vector): HBM-bound with about one flop per byte, so it runs on VALU FMAs in fp32,
+// with the loads laid out for fully coalesced 1 KiB reads (see the kernel).  Scores are
+// written as fp32 to the workspace; sequences whose budget covers every page are skipped.
 //
 // k_topk: one workgroup per (sequence, KV head) selects the k largest scores with ties
 // to the lower page index.  Scores become order-preserving uint32 keys in LDS; a radix
@@ -25,102 +21,152 @@ namespace sparrow {
 namespace {
 
 constexpr int kScoreThreads = 256;
-constexpr int kScorePagesPerWave = 64;
-constexpr int kScorePagesPerGroup = kScoreThreads / 64 * kScorePagesPerWave;  // 256
+constexpr int kScoreWaves = kScoreThreads / 64;
+constexpr int kScorePages = 32;  // pages per workgroup
+constexpr int kScoreBatch = 8;   // pages per load batch of a wave
+constexpr int kScoreHeads = 8;   // KV heads per workgroup (at most)
 constexpr int kTopkThreads = 512;
 constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kTopkBatch = 8;   // score loads in flight per thread
 
+// Sum of 8 per-lane values over the 32 lanes of a half-wave: afterwards lane i holds the
+// total of value (i & 7).  Butterfly: each xor step halves the number of values a lane
+// keeps.  Every value is summed by the same tree of commutative pairwise additions, so
+// identical inputs give identical sums wherever they sit in the batch.
+__device__ __forceinline__ float butterfly8(const float (&v)[8], int li)
+{
+    const bool b0 = li & 1, b1 = li & 2, b2 = li & 4;
+    float v1[4], v2[2];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float keep = b0 ? v[2 * j + 1] : v[2 * j];
+        const float send = b0 ? v[2 * j] : v[2 * j + 1];
+        v1[j] = keep + __shfl_xor(send, 1, 64);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const float keep = b1 ? v1[2 * j + 1] : v1[2 * j];
+        const float send = b1 ? v1[2 * j] : v1[2 * j + 1];
+        v2[j] = keep + __shfl_xor(send, 2, 64);
+    }
+    const float keep = b2 ? v2[1] : v2[0];
+    const float send = b2 ? v2[0] : v2[1];
+    float r = keep + __shfl_xor(send, 4, 64);
+    r += __shfl_xor(r, 8, 64);
+    r += __shfl_xor(r, 16, 64);
+    return r;
+}
+
+// One workgroup scores kScorePages consecutive logical pages of one sequence for up to
+// kScoreHeads KV heads.  A wave owns a pair of KV heads: each load instruction reads the
+// two heads' metadata rows of one page, 1 KiB contiguous (lanes 0-31 the first head,
+// 32-63 the second; lane i takes elements 8i..8i+7 of the 256-long row [mn | mx]).  A lane
+// multiplies its 8 bf16 elements by its 8 fp32 weights (Q- for the mn half, Q+ for the mx
+// half, built from the group's queries) in a fixed FMA chain; butterfly8 then completes
+// the dot products of a batch of 8 pages.  Batches are double-buffered in registers.
 __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ meta,
     const int32_t *__restrict__ block_table, const int32_t *__restrict__ seq_lens, Sched sched,
     int k_max, int num_q_heads, int num_kv_heads, int ps, int max_pages, float *__restrict__ scores)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t w_parts[3][2 * kHeadDim];
+    __shared__ int32_t s_phys[kScorePages];
 
-    const int unit = blockIdx.y;
-    const int b = unit / num_kv_heads;
-    const int h = unit - b * num_kv_heads;
+    const int b = blockIdx.y;
+    const int h0 = blockIdx.z * kScoreHeads;
+    const int nh = min(kScoreHeads, num_kv_heads - h0);
     const int L = clamp_len(seq_lens[b], ps, max_pages);
     const int n = (L + ps - 1) / ps;
-    const int page0 = blockIdx.x * kScorePagesPerGroup;
+    const int page0 = blockIdx.x * kScorePages;
     if (page0 >= n)
         return;
-    if (budget_pages(L, ps, sched, k_max) >= n)
-        return;  // every page is kept: nothing to score
+    const int npg = min(kScorePages, n - page0);
     const int G = num_q_heads / num_kv_heads;
     const int tid = threadIdx.x;
-
-    // Weight vector: element e < 128 multiplies mn_e, element e >= 128 multiplies mx_{e-128}.
-    {
-        const int e = tid;
-        const int i = e & (kHeadDim - 1);
-        const uint16_t *qh = q + ((int64_t)b * num_q_heads + (int64_t)h * G) * kHeadDim + i;
-        float acc = 0.f;
-        for (int g = 0; g < G; ++g) {
-            const float v = __uint_as_float((uint32_t)qh[g * kHeadDim] << 16);
-            acc += e < kHeadDim ? fminf(v, 0.f) : fmaxf(v, 0.f);
-        }
-        // acc == hi + mid + lo exactly: each remainder is exact (Sterbenz) and the three
-        // 8-bit significands cover the 24 bits of acc.
-        const uint32_t hi = to_bf16_bits(acc);
-        const float r1 = acc - __uint_as_float(hi << 16);
-        const uint32_t mid = to_bf16_bits(r1);
-        const float r2 = r1 - __uint_as_float(mid << 16);
-        const uint32_t lo = to_bf16_bits(r2);
-        w_parts[0][e] = (uint16_t)hi;
-        w_parts[1][e] = (uint16_t)mid;
-        w_parts[2][e] = (uint16_t)lo;
-    }
-    __syncthreads();
-
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
-    const int lr = lane & 15;  // A: page row; B and D: column
-    const int lg = lane >> 4;  // k sub-block of the operands; row block of D
+    const int half = lane >> 5;
+    const int li = lane & 31;
+    const int e0 = 8 * li;  // first element of this lane in the [mn | mx] row
 
-    // B operand (k = channel e, n = part): lane holds w_parts[lr][32c + 8lg .. +8) for lr < 3.
-    bf16x8_t wf[8];
+    if (tid < npg)
+        s_phys[tid] = block_table[(int64_t)b * max_pages + page0 + tid];
+
+    // Wave -> (head pair, page subset).
+    const int npairs = (nh + 1) >> 1;
+    const int wpp = kScoreWaves / npairs;  // waves sharing one head pair
+    const int pair = wave % npairs;
+    const int sub = wave / npairs;
+    const int head = 2 * pair + half;      // within the workgroup's heads
+    const bool active = sub < wpp;
+    const bool lane_on = active && head < nh;
+
+    // Weights: 8 consecutive elements of Q- (mn half) or Q+ (mx half) of this lane's head.
+    float w[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        u32x4_t v = {0u, 0u, 0u, 0u};
-        if (lr < 3)
-            v = *reinterpret_cast<const u32x4_t *>(&w_parts[lr][32 * c + 8 * lg]);
-        wf[c] = __builtin_bit_cast(bf16x8_t, v);
+    for (int j = 0; j < 8; ++j)
+        w[j] = 0.f;
+    if (lane_on) {
+        const int i0 = e0 & (kHeadDim - 1);
+        const bool neg = e0 < kHeadDim;
+        const uint16_t *qh = q + ((int64_t)b * num_q_heads + (int64_t)(h0 + head) * G) * kHeadDim + i0;
+        for (int g = 0; g < G; ++g) {
+            const u32x4_t v = ld16(qh + g * kHeadDim);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float x0 = bf16_lo(v[j]), x1 = bf16_hi(v[j]);
+                w[2 * j] += neg ? fminf(x0, 0.f) : fmaxf(x0, 0.f);
+                w[2 * j + 1] += neg ? fminf(x1, 0.f) : fmaxf(x1, 0.f);
+            }
+        }
     }
+    // Only now is the budget needed to decide whether this sequence is scored at all.
+    if (budget_pages(L, ps, sched, k_max) >= n)
+        return;  // every page is kept: nothing to score
+    __syncthreads();
+    if (!active)
+        return;
 
-    const int64_t row_stride = (int64_t)num_kv_heads * 2 * kHeadDim;  // elements per phys page
-    float *out = scores + (int64_t)unit * max_pages;
-    for (int gi = 0; gi < kScorePagesPerWave / 16; ++gi) {
-        const int base = page0 + wave * kScorePagesPerWave + gi * 16;
-        if (base >= n)
-            break;
-        const int p = base + lr;
-        u32x4_t a[8];
-        if (p < n) {
-            const int64_t phys = block_table[(int64_t)b * max_pages + p];
-            const uint16_t *row = meta + phys * row_stride + (int64_t)h * 2 * kHeadDim + 8 * lg;
+    const int64_t page_elems = (int64_t)num_kv_heads * 2 * kHeadDim;
+    const uint16_t *mbase = meta + (int64_t)(h0 + head) * 2 * kHeadDim + e0;
+    float *out = scores + ((int64_t)b * num_kv_heads + h0 + head) * max_pages + page0;
+    const int my_pages = (npg - sub + wpp - 1) / wpp;  // slots sub, sub + wpp, ...
+
+    auto load_batch = [&](int j0, u32x4_t (&v)[kScoreBatch]) {
 #pragma unroll
-            for (int c = 0; c < 8; ++c)
-                a[c] = ld16(row + 32 * c);
-        } else {
-#pragma unroll
-            for (int c = 0; c < 8; ++c)
-                a[c] = (u32x4_t){0u, 0u, 0u, 0u};
+        for (int j = 0; j < kScoreBatch; ++j) {
+            const int slot = sub + wpp * (j0 + j);
+            v[j] = (u32x4_t){0u, 0u, 0u, 0u};
+            if (j0 + j < my_pages && head < nh) {
+                const int64_t ph = __builtin_amdgcn_readfirstlane(s_phys[slot]);
+                v[j] = ld16_nt(mbase + ph * page_elems);
+            }
         }
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    };
+
+    u32x4_t nxt[kScoreBatch];
+    load_batch(0, nxt);
+    for (int j0 = 0; j0 < my_pages; j0 += kScoreBatch) {
+        u32x4_t cur[kScoreBatch];
 #pragma unroll
-        for (int c = 0; c < 8; ++c)
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[c]),
-                                                          wf[c], acc, 0, 0, 0);
-        // acc[i] = partial score of page base + 4lg + i against weight part lr.
+        for (int j = 0; j < kScoreBatch; ++j)
+            cur[j] = nxt[j];
+        if (j0 + kScoreBatch < my_pages)
+            load_batch(j0 + kScoreBatch, nxt);
+        float part[kScoreBatch];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float d1 = __shfl_down(acc[i], 1, 16);
-            const float d2 = __shfl_down(acc[i], 2, 16);
-            const int pp = base + 4 * lg + i;
-            if (lr == 0 && pp < n)
-                out[pp] = acc[i] + (d1 + d2);
+        for (int j = 0; j < kScoreBatch; ++j) {
+            float acc = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                acc = fmaf(w[2 * t], bf16_lo(cur[j][t]), acc);
+                acc = fmaf(w[2 * t + 1], bf16_hi(cur[j][t]), acc);
+            }
+            part[j] = acc;
         }
+        const float total = butterfly8(part, li);
+        const int j = j0 + (li & 7);
+        if (li < kScoreBatch && j < my_pages && head < nh)
+            out[sub + wpp * j] = total;
     }
 }
 
@@ -172,14 +218,28 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         return;
     }
 
-    // Keys into LDS; block min and max.
+    // Keys into LDS; block min and max.  Loads go out kTopkBatch at a time, independent
+    // of each other, so a sequence of up to kTopkThreads * kTopkBatch pages costs one
+    // memory round trip.
     const float *src = scores + (int64_t)unit * max_pages;
     uint32_t kmin = 0xffffffffu, kmax = 0u;
-    for (int i = tid; i < n; i += kTopkThreads) {
-        const uint32_t key = score_key(src[i]);
-        keys[i] = key;
-        kmin = min(kmin, key);
-        kmax = max(kmax, key);
+    for (int base = 0; base < n; base += kTopkThreads * kTopkBatch) {
+        float v[kTopkBatch];
+#pragma unroll
+        for (int j = 0; j < kTopkBatch; ++j) {
+            const int i = base + tid + kTopkThreads * j;
+            v[j] = i < n ? src[i] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < kTopkBatch; ++j) {
+            const int i = base + tid + kTopkThreads * j;
+            if (i < n) {
+                const uint32_t key = score_key(v[j]);
+                keys[i] = key;
+                kmin = min(kmin, key);
+                kmax = max(kmax, key);
+            }
+        }
     }
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) {
@@ -212,10 +272,17 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         for (int i = tid; i < 256; i += kTopkThreads)
             hist[i] = 0u;
         __syncthreads();
-        for (int i = tid; i < n; i += kTopkThreads) {
-            const uint32_t key = keys[i];
-            if ((key & hi_mask) == want)
-                atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        for (int base = 0; base < n; base += kTopkThreads * 4) {
+            uint32_t kv[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int i = base + tid + kTopkThreads * j;
+                kv[j] = i < n ? keys[i] : 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (base + tid + kTopkThreads * j < n && (kv[j] & hi_mask) == want)
+                    atomicAdd(&hist[(kv[j] >> shift) & 255u], 1u);
         }
         __syncthreads();
         if (wave == 0) {
@@ -299,7 +366,8 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void
 {
     float *scores = static_cast<float *>(workspace);
     const int units = s.batch * s.num_kv_heads;
-    const dim3 sgrid((s.max_pages_per_seq + kScorePagesPerGroup - 1) / kScorePagesPerGroup, units);
+    const dim3 sgrid((s.max_pages_per_seq + kScorePages - 1) / kScorePages, s.batch,
+                     (s.num_kv_heads + kScoreHeads - 1) / kScoreHeads);
     hipLaunchKernelGGL(k_page_score, sgrid, dim3(kScoreThreads), 0, stream,
                        static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
                        block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
