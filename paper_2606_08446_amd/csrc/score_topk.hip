@@ -12,9 +12,10 @@
 //
 // k_topk: one workgroup per (sequence, KV head) selects the k largest scores with ties
 // to the lower page index.  Scores become order-preserving uint32 keys in LDS; a radix
-// select over 8-bit digits (starting below the bits all keys share) finds the k-th key
-// T and how many keys equal to T to keep; one block scan of (count > T, count == T)
-// then places every kept page at its rank in ascending page order.
+// select over 8-bit digits (from the highest bit where the keys differ, stopping as soon
+// as the selection is decided) finds the threshold T and how many keys equal to T to
+// keep; one block scan of (count > T, count == T) then places every kept page at its
+// rank in ascending page order.
 #include "common.h"
 
 namespace sparrow {
@@ -196,20 +197,29 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
     int32_t *__restrict__ out_idx)
 {
     extern __shared__ uint32_t keys[];  // [max_pages]
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[2][256];
     __shared__ uint32_t red_a[kTopkWaves], red_b[kTopkWaves], red_c[kTopkWaves];
-    __shared__ uint32_t s_digit, s_rem;
+    __shared__ uint32_t s_digit, s_rem, s_done;
 
     const int unit = blockIdx.x;
     const int b = unit / num_kv_heads;
     const int h = unit - b * num_kv_heads;
     const int L = clamp_len(seq_lens[b], ps, max_pages);
     const int n = (L + ps - 1) / ps;
-    const int k = budget_pages(L, ps, sched, k_max);
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     int32_t *row = out_idx + (int64_t)unit * k_max;
+
+    // The first batch of scores is requested before the schedule lookup is resolved.
+    const float *src = scores + (int64_t)unit * max_pages;
+    float v[kTopkBatch];
+#pragma unroll
+    for (int j = 0; j < kTopkBatch; ++j) {
+        const int i = tid + kTopkThreads * j;
+        v[j] = i < n ? src[i] : 0.f;
+    }
+    const int k = budget_pages(L, ps, sched, k_max);
     if (h == 0 && tid == 0)
         out_k[b] = k;
     if (k >= n) {  // every page kept (also n == 0)
@@ -218,17 +228,15 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         return;
     }
 
-    // Keys into LDS; block min and max.  Loads go out kTopkBatch at a time, independent
-    // of each other, so a sequence of up to kTopkThreads * kTopkBatch pages costs one
-    // memory round trip.
-    const float *src = scores + (int64_t)unit * max_pages;
+    // Keys into LDS; block min and max.
     uint32_t kmin = 0xffffffffu, kmax = 0u;
     for (int base = 0; base < n; base += kTopkThreads * kTopkBatch) {
-        float v[kTopkBatch];
+        if (base > 0) {
 #pragma unroll
-        for (int j = 0; j < kTopkBatch; ++j) {
-            const int i = base + tid + kTopkThreads * j;
-            v[j] = i < n ? src[i] : 0.f;
+            for (int j = 0; j < kTopkBatch; ++j) {
+                const int i = base + tid + kTopkThreads * j;
+                v[j] = i < n ? src[i] : 0.f;
+            }
         }
 #pragma unroll
         for (int j = 0; j < kTopkBatch; ++j) {
@@ -241,6 +249,8 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
             }
         }
     }
+    for (int t = tid; t < 256; t += kTopkThreads)
+        hist[0][t] = 0u;
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) {
         kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
@@ -259,62 +269,86 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         kmax = max(kmax, red_b[w]);
     }
 
-    // Radix select of the k-th largest key T, MSB digit first.  Bits above the highest
-    // bit where kmin and kmax differ are shared by every key.
+    // Radix select of the k-th largest key, 8-bit digits from the highest bit where the
+    // keys differ down (the bits above it are common to all keys).  After each digit the
+    // candidates are the keys whose bits >= lo equal `prefix`; `rem` of them are still to be
+    // taken.  When the chosen bin holds exactly `rem` keys every candidate is taken and the
+    // selection is "bits >= lo at least prefix", with no tie left to break.
     uint32_t prefix = kmax;
-    uint32_t rem = (uint32_t)k;  // keys still to take among those matching the prefix
-    int shift = -8;
-    if (kmin != kmax)
-        shift = ((31 - __builtin_clz(kmin ^ kmax)) >> 3) << 3;
-    for (; shift >= 0; shift -= 8) {
-        const uint32_t hi_mask = shift >= 24 ? 0u : (0xffffffffu << (shift + 8));
-        const uint32_t want = prefix & hi_mask;
-        for (int i = tid; i < 256; i += kTopkThreads)
-            hist[i] = 0u;
-        __syncthreads();
-        for (int base = 0; base < n; base += kTopkThreads * 4) {
-            uint32_t kv[4];
+    uint32_t rem = (uint32_t)k;
+    bool exact = true;  // false: stopped early, keep keys >= prefix (bits below lo zero)
+    int lo = 0;
+    if (kmin != kmax) {
+        int hi = 31 - __builtin_clz(kmin ^ kmax);
+        int cur = 0;
+        while (hi >= 0) {
+            lo = hi >= 7 ? hi - 7 : 0;
+            const uint32_t width_mask = (1u << (hi - lo + 1)) - 1u;
+            const uint32_t above = hi >= 31 ? 0u : (0xffffffffu << (hi + 1));
+            const uint32_t want = prefix & above;
+            for (int base = 0; base < n; base += kTopkThreads * 4) {
+                uint32_t kv[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int i = base + tid + kTopkThreads * j;
-                kv[j] = i < n ? keys[i] : 0u;
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (base + tid + kTopkThreads * j < n && (kv[j] & hi_mask) == want)
-                    atomicAdd(&hist[(kv[j] >> shift) & 255u], 1u);
-        }
-        __syncthreads();
-        if (wave == 0) {
-            // lane l owns digits 255-4l .. 252-4l; counts accumulate from the top digit down
-            const uint32_t c0 = hist[255 - 4 * lane], c1 = hist[254 - 4 * lane];
-            const uint32_t c2 = hist[253 - 4 * lane], c3 = hist[252 - 4 * lane];
-            const uint32_t tot = c0 + c1 + c2 + c3;
-            const uint32_t incl = wave_inclusive_scan(tot, lane);
-            uint32_t acc = incl - tot;  // keys with a larger digit
-            if (acc < rem && rem <= incl) {
-                int d;
-                if (rem <= acc + c0) {
-                    d = 255 - 4 * lane;
-                } else if (rem <= acc + c0 + c1) {
-                    acc += c0;
-                    d = 254 - 4 * lane;
-                } else if (rem <= acc + c0 + c1 + c2) {
-                    acc += c0 + c1;
-                    d = 253 - 4 * lane;
-                } else {
-                    acc += c0 + c1 + c2;
-                    d = 252 - 4 * lane;
+                for (int j = 0; j < 4; ++j) {
+                    const int i = base + tid + kTopkThreads * j;
+                    kv[j] = i < n ? keys[i] : 0u;
                 }
-                s_digit = (uint32_t)d;
-                s_rem = rem - acc;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (base + tid + kTopkThreads * j < n && (kv[j] & above) == want)
+                        atomicAdd(&hist[cur][(kv[j] >> lo) & width_mask], 1u);
             }
+            for (int t = tid; t < 256; t += kTopkThreads)
+                hist[cur ^ 1][t] = 0u;  // ready for the next digit
+            __syncthreads();
+            if (wave == 0) {
+                // lane l owns digits 255-4l .. 252-4l; counts accumulate from the top down
+                const uint32_t c0 = hist[cur][255 - 4 * lane], c1 = hist[cur][254 - 4 * lane];
+                const uint32_t c2 = hist[cur][253 - 4 * lane], c3 = hist[cur][252 - 4 * lane];
+                const uint32_t tot = c0 + c1 + c2 + c3;
+                const uint32_t incl = wave_inclusive_scan(tot, lane);
+                uint32_t acc = incl - tot;  // keys with a larger digit
+                if (acc < rem && rem <= incl) {
+                    int d;
+                    uint32_t cnt;
+                    if (rem <= acc + c0) {
+                        d = 255 - 4 * lane;
+                        cnt = c0;
+                    } else if (rem <= acc + c0 + c1) {
+                        acc += c0;
+                        d = 254 - 4 * lane;
+                        cnt = c1;
+                    } else if (rem <= acc + c0 + c1 + c2) {
+                        acc += c0 + c1;
+                        d = 253 - 4 * lane;
+                        cnt = c2;
+                    } else {
+                        acc += c0 + c1 + c2;
+                        d = 252 - 4 * lane;
+                        cnt = c3;
+                    }
+                    s_digit = (uint32_t)d;
+                    s_rem = rem - acc;
+                    s_done = cnt == rem - acc;
+                }
+            }
+            __syncthreads();
+            prefix = want | (s_digit << lo);
+            rem = s_rem;
+            if (s_done) {
+                exact = false;
+                break;
+            }
+            hi = lo - 1;
+            cur ^= 1;
         }
-        __syncthreads();
-        prefix = want | (s_digit << shift);
-        rem = s_rem;
     }
-    const uint32_t T = prefix;  // k-th largest key; keep every key > T and `rem` keys == T
+    // Selection rule as "key > T" plus the first `rem` keys equal to T in page order.
+    uint32_t T = prefix;
+    if (!exact) {
+        T = prefix - 1u;  // keys >= prefix (prefix > 0 here, as fewer than n keys are kept)
+        rem = 0u;
+    }
 
     // Ranks: a kept page's position is (#keys > T before it) + min(#keys == T before it, rem).
     const int seg = (n + kTopkThreads - 1) / kTopkThreads;
@@ -375,8 +409,8 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    const size_t lds = (size_t)s.max_pages_per_seq * sizeof(uint32_t);
-    hipLaunchKernelGGL(k_topk, dim3(units), dim3(kTopkThreads), lds, stream, scores, seq_lens,
+    hipLaunchKernelGGL(k_topk, dim3(units), dim3(kTopkThreads),
+                       (size_t)s.max_pages_per_seq * sizeof(uint32_t), stream, scores, seq_lens,
                        sched, k_max, s.num_kv_heads, s.page_size, s.max_pages_per_seq, out_k,
                        out_idx);
     return hipGetLastError();

@@ -314,3 +314,35 @@ def test_full_size_c5_append_and_update():
     np.testing.assert_array_equal(W.bf16_bits(meta)[h["phys"]],
                                   oracle.page_meta(h["k"], h["bt"], h["lens"]))
     sampled_check(inp, seqs, bound(inp), dense=False, label="c5 after append")
+
+
+def test_workspace_reuse_across_sizes():
+    log("case workspace reuse")
+    inp = small_inputs(4, 2, 16, (9000, 3000, 700), seed=19, schedule=W.fraction_budget(1, 3))
+    shape = S.shape_of(inp.q, inp.k_cache, inp.block_table)
+    k_max = inp.max_pages
+    # one workspace of each kind, left uninitialised, reused by every call below
+    ws = torch.empty(S.sparrow_workspace_size(shape, k_max, S.SPARROW_OP_SPARSE_ATTN),
+                     dtype=torch.uint8, device=DEV)
+    dws = torch.empty(S.sparrow_workspace_size(shape, 0, S.SPARROW_OP_DENSE_ATTN),
+                      dtype=torch.uint8, device=DEV)
+    h = host(inp)
+    n = np.array([(int(L) + 15) // 16 for L in h["lens"]], np.int32)
+    rng = np.random.default_rng(0)
+    for trial, frac in enumerate((1.0, 0.3, 0.05, 1.0)):
+        kk = np.maximum(1, np.ceil(n * frac)).astype(np.int32)
+        idx = np.full((3, 2, k_max), -1, np.int32)
+        for b in range(3):
+            for hh in range(2):
+                idx[b, hh, :kk[b]] = np.sort(rng.choice(n[b], size=kk[b], replace=False))
+        out = S.sparse_decode_attn(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+                                   torch.as_tensor(kk, device=DEV), torch.as_tensor(idx, device=DEV),
+                                   SCALE, workspace=ws)
+        dense = S.dense_decode_attn(inp.q, inp.k_cache, inp.v_cache, inp.block_table,
+                                    inp.seq_lens, SCALE, workspace=dws)
+        torch.cuda.synchronize()
+        ref = oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], SCALE, kk, idx)
+        check_out(out.cpu().numpy().astype(np.float64), ref, f"reuse sparse {trial}")
+        if trial == 0:
+            ref_d = oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], SCALE)
+        check_out(dense.cpu().numpy().astype(np.float64), ref_d, f"reuse dense {trial}")
