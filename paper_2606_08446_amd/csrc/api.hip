@@ -94,9 +94,9 @@ int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, cons
         return SPARROW_EUNSUPPORTED;
     if (shape->batch == 0)
         return SPARROW_OK;
-    const AttnPlan plan = plan_attention(*shape, k_max);
-    if (plan.max_splits > 65535 || (int64_t)shape->batch * shape->num_kv_heads > 65535)
-        return SPARROW_EINVAL;
+    if (shape->batch > kAttnMaxBatch)
+        return SPARROW_EUNSUPPORTED;
+    const AttnPlan plan = plan_attention(*shape);
     if (!workspace || ws_bytes < plan.workspace_bytes)
         return SPARROW_EWORKSPACE;
     return status_of(launch_attention(*shape, plan, q, k_cache, v_cache, block_table, seq_lens, k,
@@ -118,9 +118,9 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
         return SPARROW_EUNSUPPORTED;
     if (shape->batch == 0)
         return SPARROW_OK;
-    const AttnPlan plan = plan_attention(*shape, shape->max_pages_per_seq);
-    if (plan.max_splits > 65535 || (int64_t)shape->batch * shape->num_kv_heads > 65535)
-        return SPARROW_EINVAL;
+    if (shape->batch > kAttnMaxBatch)
+        return SPARROW_EUNSUPPORTED;
+    const AttnPlan plan = plan_attention(*shape);
     if (!workspace || ws_bytes < plan.workspace_bytes)
         return SPARROW_EWORKSPACE;
     return status_of(launch_attention(*shape, plan, q, k_cache, v_cache, block_table, seq_lens,
@@ -134,9 +134,10 @@ size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32
         return 0;
     switch (op) {
     case SPARROW_OP_SCORE_TOPK: return score_topk_workspace(*shape);
-    case SPARROW_OP_SPARSE_ATTN: return k_max < 1 ? 0 : plan_attention(*shape, k_max).workspace_bytes;
+    case SPARROW_OP_SPARSE_ATTN:
+        return k_max < 1 || shape->batch > kAttnMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
     case SPARROW_OP_DENSE_ATTN:
-        return plan_attention(*shape, shape->max_pages_per_seq).workspace_bytes;
+        return shape->batch > kAttnMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
     default: return 0;
     }
 }

@@ -2,11 +2,15 @@
 // the attention term of the cost models of Sec. 3.3 (Eq. dense-cost, Eq. sparse-cost) of
 // arXiv 2606.08446, with the block-sparse token set of Sec. 2.
 //
-// Work split: one workgroup (4 waves) per (sequence, KV head, split), a split being up to
-// `pages_per_split` consecutive entries of the page list (the top-k list, or 0..n-1).  The
-// waves of a workgroup take the split's pages round-robin and run an online softmax over
-// 16-token chunks; their states are merged in LDS and written as one partial (m, l, o).
-// k_combine merges the partials of a (sequence, query head) with log-sum-exp weights.
+// Work split (streaming waves).  All (sequence, KV head, listed page) positions are laid
+// end to end - sequence by sequence, head by head, in list order - and every resident
+// wave takes one equal, contiguous range of them.  A wave streams its range chunk by
+// chunk with the next 16-token chunk's K/V loads always in flight, and the page list is
+// prefetched in batches of 64 pages one batch ahead, across (sequence, head) boundaries.
+// Its online-softmax state is flushed whenever its range leaves a (sequence, KV head):
+// a unit whose pages all fall in one wave is normalised and written to `out` directly;
+// otherwise the wave writes a partial (m, l, o) to segment slot `wave + unit` (unique
+// along the partition) and k_attn_merge combines the partials of that unit.
 //
 // Per 16-token chunk, one wave computes all G <= 16 query heads of its KV head on MFMA:
 //   QK:  D[t][g] = sum_d K[t][d] q[g][d]  - 4 x mfma_f32_16x16x32_bf16
@@ -27,9 +31,24 @@ namespace {
 
 constexpr int kAttnThreads = 256;
 constexpr int kAttnWaves = kAttnThreads / 64;
-constexpr int kMaxPagesPerSplit = 64;
-constexpr int kTokensPerSplit = 512;
-constexpr int kOStride = kHeadDim + 4;  // LDS row stride of the wave merge (bank spread)
+constexpr int kBatch = 64;        // pages per prefetched page-list batch
+constexpr int kMaxWaves = 4096;   // upper bound of streaming waves (sizes the workspace)
+
+struct AttnArgs {
+    const uint16_t *q;
+    const uint16_t *k_cache;
+    const uint16_t *v_cache;
+    const int32_t *block_table;
+    const int32_t *seq_lens;
+    const int32_t *ksel;
+    const int32_t *idx;
+    int32_t *plan_off;  // [batch + 1] page offsets of the sequences (written by workgroup 0)
+    float *o_part;
+    float *ml_part;
+    void *out;
+    int k_max, batch, num_q_heads, num_kv_heads, ps, max_pages, out_bf16, total_waves;
+    float scale_log2;
+};
 
 struct Chunk {
     u32x4_t k[4];  // A operand of the 4 QK instructions
@@ -57,85 +76,188 @@ __device__ __forceinline__ uint32_t pair_of(u32x4_t x, u32x4_t y, int c)
                    : __builtin_amdgcn_perm(b, a, 0x05040100u);
 }
 
-template <bool kSparse>
-__global__ __launch_bounds__(kAttnThreads) void k_attn_split(
-    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k_cache,
-    const uint16_t *__restrict__ v_cache, const int32_t *__restrict__ block_table,
-    const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ ksel,
-    const int32_t *__restrict__ idx, int k_max, int num_q_heads, int num_kv_heads, int ps,
-    int max_pages, int pages_per_split, int max_splits, float scale_log2,
-    float *__restrict__ o_part, float *__restrict__ ml_part)
+__device__ __forceinline__ void store_out(void *out, int out_bf16, int64_t i, float v)
 {
-    __shared__ int32_t s_phys[kMaxPagesPerSplit];
-    __shared__ int32_t s_tok0[kMaxPagesPerSplit];
-    __shared__ float s_m[kAttnWaves][16];
-    __shared__ float s_l[kAttnWaves][16];
-    __shared__ float s_o[kAttnWaves][16][kOStride];
+    if (out_bf16)
+        static_cast<uint16_t *>(out)[i] = (uint16_t)to_bf16_bits(v);
+    else
+        static_cast<float *>(out)[i] = v;
+}
 
-    const int unit = blockIdx.y;
-    const int split = blockIdx.x;
-    const int b = unit / num_kv_heads;
-    const int h = unit - b * num_kv_heads;
-    const int G = num_q_heads / num_kv_heads;
-    const int L = clamp_len(seq_lens[b], ps, max_pages);
-    const int n = (L + ps - 1) / ps;
-    int count = n;
-    if (kSparse) {
-        count = ksel[b];
-        count = count < 0 ? 0 : (count > k_max ? k_max : count);
-    }
-    const int j0 = split * pages_per_split;
-    if (j0 >= count)
-        return;
-    const int npg = min(pages_per_split, count - j0);
+// Pages in the attention list of sequence b.
+template <bool kSparse>
+__device__ __forceinline__ int list_pages(const AttnArgs &a, int b)
+{
+    const int L = clamp_len(a.seq_lens[b], a.ps, a.max_pages);
+    const int n = (L + a.ps - 1) / a.ps;
+    if (!kSparse)
+        return n;
+    const int c = a.ksel[b];
+    return c < 0 ? 0 : (c > a.k_max ? a.k_max : c);
+}
+
+// Block-wide exclusive prefix of list_pages over the batch into s_off[0 .. batch].
+template <bool kSparse>
+__device__ void seq_prefix(const AttnArgs &a, int32_t *s_off, int32_t *s_tmp)
+{
     const int tid = threadIdx.x;
-    if (tid < npg) {
-        const int lp = kSparse ? idx[(int64_t)unit * k_max + j0 + tid] : j0 + tid;
-        int ph = -1;
-        if (lp >= 0 && lp < n)
-            ph = block_table[(int64_t)b * max_pages + lp];
-        s_phys[tid] = ph;
-        s_tok0[tid] = lp * ps;
-    }
-
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int B = a.batch;
+    const int per = (B + kAttnThreads - 1) / kAttnThreads;
+    const int b0 = min(B, tid * per);
+    const int b1 = min(B, b0 + per);
+    int local = 0;
+    for (int b = b0; b < b1; ++b)
+        local += list_pages<kSparse>(a, b);
+    int incl = local;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int t = __shfl_up(incl, d, 64);
+        if (lane >= d)
+            incl += t;
+    }
+    if (lane == 63)
+        s_tmp[wave] = incl;
+    __syncthreads();
+    int run = incl - local;
+    for (int w = 0; w < wave; ++w)
+        run += s_tmp[w];
+    for (int b = b0; b < b1; ++b) {
+        s_off[b] = run;
+        run += list_pages<kSparse>(a, b);
+    }
+    if (tid == kAttnThreads - 1)
+        s_off[B] = run;  // this thread's range ends at B (or is empty): run is the total
+    __syncthreads();
+}
+
+// Position cursor over the (sequence, head, page) list.
+struct Cursor {
+    int b, h, j, cnt;  // sequence, KV head, page position within the unit, unit length
+    int64_t pos;       // global position
+};
+
+// One page-list batch of at most kBatch pages of one unit; lane i describes page j0 + i.
+struct Batch {
+    int b, h, j0, n, L;
+    bool ends_unit;
+    int phys;  // physical page (-1: entry outside the sequence)
+    int tok0;  // first token of the page
+};
+
+template <bool kSparse>
+__device__ __forceinline__ void fetch_batch(const AttnArgs &a, const int32_t *s_off, Cursor &c,
+                                            int64_t pos_end, Batch &t, int lane)
+{
+    const int Hkv = a.num_kv_heads;
+    t.b = c.b;
+    t.h = c.h;
+    t.j0 = c.j;
+    const int64_t left = pos_end - c.pos;
+    int n = c.cnt - c.j;
+    if (n > kBatch)
+        n = kBatch;
+    if (n > left)
+        n = (int)left;
+    t.n = n;
+    t.ends_unit = c.j + n == c.cnt;
+    t.L = clamp_len(a.seq_lens[c.b], a.ps, a.max_pages);
+    const int np = (t.L + a.ps - 1) / a.ps;
+    t.phys = -1;
+    t.tok0 = 0;
+    if (lane < n) {
+        const int lp = kSparse ? a.idx[((int64_t)c.b * Hkv + c.h) * a.k_max + c.j + lane]
+                               : c.j + lane;
+        if (lp >= 0 && lp < np)
+            t.phys = a.block_table[(int64_t)c.b * a.max_pages + lp];
+        t.tok0 = lp * a.ps;
+    }
+    c.pos += n;
+    c.j += n;
+    if (c.j == c.cnt && c.pos < pos_end) {  // next unit with pages
+        c.j = 0;
+        if (++c.h == Hkv) {
+            c.h = 0;
+            do {
+                ++c.b;
+            } while (s_off[c.b + 1] == s_off[c.b]);
+        }
+        c.cnt = s_off[c.b + 1] - s_off[c.b];
+    }
+}
+
+__device__ __forceinline__ void load_q(const AttnArgs &a, int b, int h, int lr, int lg,
+                                       bf16x8_t (&qf)[4])
+{
+    const int G = a.num_q_heads / a.num_kv_heads;
+    const uint16_t *qrow = a.q + ((int64_t)b * a.num_q_heads + (int64_t)h * G + lr) * kHeadDim;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        u32x4_t v = {0u, 0u, 0u, 0u};
+        if (lr < G)
+            v = ld16(qrow + 32 * i + 8 * lg);
+        qf[i] = __builtin_bit_cast(bf16x8_t, v);
+    }
+}
+
+template <bool kSparse>
+__global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
+{
+    extern __shared__ int32_t s_off[];  // [batch + 1]
+    __shared__ int32_t s_tmp[kAttnWaves];
+
+    seq_prefix<kSparse>(a, s_off, s_tmp);
+    const int B = a.batch;
+    const int Hkv = a.num_kv_heads;
+    const int G = a.num_q_heads / Hkv;
+    if (blockIdx.x == 0)
+        for (int b = threadIdx.x; b <= B; b += kAttnThreads)
+            a.plan_off[b] = s_off[b];
+
+    const int64_t P = (int64_t)s_off[B] * Hkv;
+    const int64_t W = P < a.total_waves ? P : a.total_waves;
+    const int w = blockIdx.x * kAttnWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= W)
+        return;
+    const int64_t pos_begin = (int64_t)w * P / W;
+    const int64_t pos_end = (int64_t)(w + 1) * P / W;
+    const int lane = threadIdx.x & 63;
     const int lr = lane & 15;
     const int lg = lane >> 4;
-
-    // B operand of QK: lane (g = lr, r = lg) holds q[g][32i + 8r .. +8) for instruction i.
-    bf16x8_t qf[4];
-    {
-        const uint16_t *qrow = q + ((int64_t)b * num_q_heads + (int64_t)h * G + lr) * kHeadDim;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            u32x4_t v = {0u, 0u, 0u, 0u};
-            if (lr < G)
-                v = ld16(qrow + 32 * i + 8 * lg);
-            qf[i] = __builtin_bit_cast(bf16x8_t, v);
-        }
-    }
-    __syncthreads();
-
+    const int ps = a.ps;
     const int cpp = ps >> 4;  // 16-token chunks per page
-    const int my_pages = npg > wave ? (npg - wave + kAttnWaves - 1) / kAttnWaves : 0;
-    const int n_it = my_pages * cpp;
     const int64_t head_elems = (int64_t)ps * kHeadDim;
 
-    // Chunk `it` of this wave: page slot wave + 4 * (it / cpp), sub-chunk it % cpp.
-    auto chunk_info = [&](int it, int64_t &off, int &tok0) -> bool {
-        const int slot = wave + kAttnWaves * (it / cpp);
-        const int sub = it - (it / cpp) * cpp;
-        const int ph = __builtin_amdgcn_readfirstlane(s_phys[slot]);
-        tok0 = __builtin_amdgcn_readfirstlane(s_tok0[slot]) + 16 * sub;
-        off = ((int64_t)ph * num_kv_heads + h) * head_elems + (int64_t)(16 * sub) * kHeadDim;
-        return ph >= 0 && tok0 < L;
-    };
-    auto next_live = [&](int it, int64_t &off, int &tok0) -> int {
-        while (it < n_it && !chunk_info(it, off, tok0))
-            ++it;
-        return it;
-    };
+    // Locate the first position: the last sequence whose offset is <= pos_begin is the one
+    // holding it (empty sequences before it share its offset).
+    Cursor cur;
+    {
+        int lo = 0, hi = B - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)s_off[mid] * Hkv <= pos_begin)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        cur.b = lo;
+        cur.cnt = s_off[lo + 1] - s_off[lo];
+        const int64_t rel = pos_begin - (int64_t)s_off[lo] * Hkv;
+        cur.h = (int)(rel / cur.cnt);
+        cur.j = (int)(rel - (int64_t)cur.h * cur.cnt);
+        cur.pos = pos_begin;
+    }
+
+    Batch bc, bn;
+    fetch_batch<kSparse>(a, s_off, cur, pos_end, bc, lane);
+    bool have_next = cur.pos < pos_end;
+    if (have_next)
+        fetch_batch<kSparse>(a, s_off, cur, pos_end, bn, lane);
+
+    bf16x8_t qf[4], qn[4];
+    load_q(a, bc.b, bc.h, lr, lg, qf);
+    bool from_start = bc.j0 == 0;
 
     float m_run = -INFINITY;
     float l_run = 0.f;
@@ -144,164 +266,219 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_split(
     for (int c = 0; c < 8; ++c)
         O[c] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-    int64_t off_next = 0;
-    int tok_next = 0;
-    int it = next_live(0, off_next, tok_next);
+    // chunk `ci` of batch t: page ci / cpp, sub-chunk ci % cpp
+    auto issue = [&](const Batch &t, int ci, Chunk &ch, int &tok) -> bool {
+        const int pi = ci / cpp;
+        const int sub = ci - pi * cpp;
+        const int ph = __builtin_amdgcn_readlane(t.phys, pi);
+        tok = __builtin_amdgcn_readlane(t.tok0, pi) + 16 * sub;
+        const bool live = ph >= 0 && tok < t.L;
+        if (live) {
+            const int64_t off =
+                ((int64_t)ph * Hkv + t.h) * head_elems + (int64_t)(16 * sub) * kHeadDim;
+            load_chunk(ch, a.k_cache + off, a.v_cache + off, lr, lg);
+        }
+        return live;
+    };
+
     Chunk nxt;
-    if (it < n_it)
-        load_chunk(nxt, k_cache + off_next, v_cache + off_next, lr, lg);
-    while (it < n_it) {
-        Chunk cur = nxt;
+    int tok_next = 0;
+    bool live_next = issue(bc, 0, nxt, tok_next);
+    int ci = 0;
+    for (;;) {
+        Chunk ch = nxt;
+        const bool live = live_next;
         const int tok0 = tok_next;
-        it = next_live(it + 1, off_next, tok_next);
-        if (it < n_it)
-            load_chunk(nxt, k_cache + off_next, v_cache + off_next, lr, lg);
-
-        // ---- logits of 16 tokens x 16 (padded) heads
-        f32x4_t s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.k[i]),
-                                                        qf[i], s, 0, 0, 0);
-        const int valid = L - tok0;  // >= 1
-        float z[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            z[i] = (4 * lg + i < valid) ? s[i] * scale_log2 : -INFINITY;
-        float cm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
-        cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
-        cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
-        const float m_new = fmaxf(m_run, cm);
-        const float alpha = exp2f(m_run - m_new);
-        const uint32_t p01 = pack_bf16(exp2f(z[0] - m_new), exp2f(z[1] - m_new));
-        const uint32_t p23 = pack_bf16(exp2f(z[2] - m_new), exp2f(z[3] - m_new));
-        l_run = l_run * alpha + ((bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23)));
-        m_run = m_new;
-        if (__ballot(alpha != 1.f)) {
-#pragma unroll
-            for (int c = 0; c < 8; ++c)
-                O[c] *= alpha;
+        const int L = bc.L;
+        const bool last_in_batch = ci + 1 == bc.n * cpp;
+        if (!last_in_batch) {
+            live_next = issue(bc, ci + 1, nxt, tok_next);
+        } else if (have_next) {
+            live_next = issue(bn, 0, nxt, tok_next);
+            if (bc.ends_unit)
+                load_q(a, bn.b, bn.h, lr, lg, qn);
         }
-        if (valid < 16) {  // tokens past the length: zero V (cache slots may hold anything)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (4 * lg + j >= valid)
-                    cur.v[j] = (u32x4_t){0u, 0u, 0u, 0u};
-        }
-        // ---- O^T += V^T P
-        const s16x4_t pb = __builtin_bit_cast(s16x4_t, (u32x2_t){p01, p23});
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            const u32x2_t a = {pair_of(cur.v[0], cur.v[1], c), pair_of(cur.v[2], cur.v[3], c)};
-            O[c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a), pb,
-                                                             O[c], 0, 0, 0);
-        }
-    }
 
-    // ---- merge the waves of the workgroup
-    l_run += __shfl_xor(l_run, 16, 64);
-    l_run += __shfl_xor(l_run, 32, 64);
-    if (lg == 0) {
-        s_m[wave][lr] = m_run;
-        s_l[wave][lr] = l_run;
-    }
+        if (live) {
+            // ---- logits of 16 tokens x 16 (padded) heads
+            f32x4_t s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
+            for (int i = 0; i < 4; ++i)
+                s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ch.k[i]),
+                                                            qf[i], s, 0, 0, 0);
+            const int valid = L - tok0;  // >= 1
+            float z[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            s_o[wave][lr][32 * lg + 8 * i + c] = O[c][i];
-    __syncthreads();
-
-    const int64_t pbase = (int64_t)unit * max_splits + split;
-    for (int e = tid; e < G * kHeadDim; e += kAttnThreads) {
-        const int g = e >> 7;
-        const int d = e & (kHeadDim - 1);
-        float M = s_m[0][g];
+            for (int i = 0; i < 4; ++i)
+                z[i] = (4 * lg + i < valid) ? s[i] * a.scale_log2 : -INFINITY;
+            float cm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+            cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
+            cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+            const float m_new = fmaxf(m_run, cm);
+            const float alpha = exp2f(m_run - m_new);
+            const uint32_t p01 = pack_bf16(exp2f(z[0] - m_new), exp2f(z[1] - m_new));
+            const uint32_t p23 = pack_bf16(exp2f(z[2] - m_new), exp2f(z[3] - m_new));
+            l_run = l_run * alpha + ((bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23)));
+            m_run = m_new;
+            if (__ballot(alpha != 1.f)) {
 #pragma unroll
-        for (int w = 1; w < kAttnWaves; ++w)
-            M = fmaxf(M, s_m[w][g]);
-        float acc = 0.f, lsum = 0.f;
-        if (M != -INFINITY) {
+                for (int c = 0; c < 8; ++c)
+                    O[c] *= alpha;
+            }
+            if (valid < 16) {  // tokens past the length: zero V (cache slots may hold anything)
 #pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w) {
-                const float f = exp2f(s_m[w][g] - M);
-                acc += f * s_o[w][g][d];
-                lsum += f * s_l[w][g];
+                for (int j = 0; j < 4; ++j)
+                    if (4 * lg + j >= valid)
+                        ch.v[j] = (u32x4_t){0u, 0u, 0u, 0u};
+            }
+            // ---- O^T += V^T P
+            const s16x4_t pb = __builtin_bit_cast(s16x4_t, (u32x2_t){p01, p23});
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const u32x2_t av = {pair_of(ch.v[0], ch.v[1], c), pair_of(ch.v[2], ch.v[3], c)};
+                O[c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, av),
+                                                                 pb, O[c], 0, 0, 0);
             }
         }
-        o_part[(pbase * G + g) * kHeadDim + d] = acc;
-        if (d == 0) {
-            ml_part[(pbase * G + g) * 2 + 0] = M;
-            ml_part[(pbase * G + g) * 2 + 1] = lsum;
+
+        if (!last_in_batch) {
+            ++ci;
+            continue;
         }
+        if (bc.ends_unit || !have_next) {
+            // ---- flush the unit's state: the output itself, or a partial for the merge
+            float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+            l_tot += __shfl_xor(l_tot, 32, 64);
+            const int unit = bc.b * Hkv + bc.h;
+            if (lr < G) {
+                if (from_start && bc.ends_unit) {
+                    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+                    const int64_t orow =
+                        ((int64_t)bc.b * a.num_q_heads + (int64_t)bc.h * G + lr) * kHeadDim;
+#pragma unroll
+                    for (int c = 0; c < 8; ++c)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            store_out(a.out, a.out_bf16, orow + 32 * lg + 8 * i + c,
+                                      O[c][i] * inv);
+                } else {
+                    const int64_t seg = (int64_t)w + unit;
+                    float *op = a.o_part + (seg * G + lr) * kHeadDim + 32 * lg;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        st16(op + 8 * i, __builtin_bit_cast(
+                                             u32x4_t, (f32x4_t){O[0][i], O[1][i], O[2][i], O[3][i]}));
+                        st16(op + 8 * i + 4, __builtin_bit_cast(u32x4_t, (f32x4_t){O[4][i], O[5][i],
+                                                                                  O[6][i], O[7][i]}));
+                    }
+                    if (lg == 0) {
+                        a.ml_part[(seg * G + lr) * 2 + 0] = m_run;
+                        a.ml_part[(seg * G + lr) * 2 + 1] = l_tot;
+                    }
+                }
+            }
+            if (!have_next)
+                break;
+            m_run = -INFINITY;
+            l_run = 0.f;
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+                O[c] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                qf[i] = qn[i];
+            from_start = bn.j0 == 0;
+        }
+        bc = bn;
+        ci = 0;
+        have_next = cur.pos < pos_end;
+        if (have_next)
+            fetch_batch<kSparse>(a, s_off, cur, pos_end, bn, lane);
     }
 }
 
-__global__ __launch_bounds__(kHeadDim) void k_combine(
-    const float *__restrict__ o_part, const float *__restrict__ ml_part,
-    const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ ksel, int k_max,
-    int sparse, int num_q_heads, int num_kv_heads, int ps, int max_pages, int pages_per_split,
-    int max_splits, void *__restrict__ out, int out_bf16)
+// Merges the partials of a (sequence, KV head) that spans several waves, and writes zero
+// rows for sequences without pages.  One 128-thread workgroup per (sequence, KV head),
+// thread = channel; one pass over the unit's segments with a running maximum.
+__global__ __launch_bounds__(kHeadDim) void k_attn_merge(AttnArgs a)
 {
-    const int bj = blockIdx.x;
-    const int b = bj / num_q_heads;
-    const int j = bj - b * num_q_heads;
-    const int G = num_q_heads / num_kv_heads;
-    const int h = j / G;
-    const int g = j - h * G;
-    const int unit = b * num_kv_heads + h;
+    const int unit = blockIdx.x;
+    const int Hkv = a.num_kv_heads;
+    const int b = unit / Hkv;
+    const int h = unit - b * Hkv;
+    const int G = a.num_q_heads / Hkv;
     const int d = threadIdx.x;
-    const int L = clamp_len(seq_lens[b], ps, max_pages);
-    int count = (L + ps - 1) / ps;
-    if (sparse) {
-        count = ksel[b];
-        count = count < 0 ? 0 : (count > k_max ? k_max : count);
+    const int64_t cnt = a.plan_off[b + 1] - a.plan_off[b];
+    const int64_t orow = ((int64_t)b * a.num_q_heads + (int64_t)h * G) * kHeadDim + d;
+    if (cnt == 0) {
+        for (int g = 0; g < G; ++g)
+            store_out(a.out, a.out_bf16, orow + (int64_t)g * kHeadDim, 0.f);
+        return;
     }
-    const int n_splits = (count + pages_per_split - 1) / pages_per_split;
-    const float *ml = ml_part + ((int64_t)unit * max_splits * G + g) * 2;
-    const float *op = o_part + ((int64_t)unit * max_splits * G + g) * kHeadDim + d;
-    float M = -INFINITY;
-    for (int s = 0; s < n_splits; ++s)
-        M = fmaxf(M, ml[(int64_t)s * G * 2]);
-    float result = 0.f;
-    if (M != -INFINITY) {
-        float acc = 0.f, lsum = 0.f;
-        for (int s = 0; s < n_splits; ++s) {
-            const float f = exp2f(ml[(int64_t)s * G * 2] - M);
-            acc += f * op[(int64_t)s * G * kHeadDim];
-            lsum += f * ml[(int64_t)s * G * 2 + 1];
+    const int64_t P = (int64_t)a.plan_off[a.batch] * Hkv;
+    const int64_t W = P < a.total_waves ? P : a.total_waves;
+    const int64_t off = (int64_t)a.plan_off[b] * Hkv + h * cnt;
+    const int64_t wf = ((off + 1) * W - 1) / P;    // wave holding the unit's first page
+    const int64_t wl = ((off + cnt) * W - 1) / P;  // wave holding its last page
+    if (wf == wl)
+        return;  // one wave held the whole unit and wrote its output
+    for (int g = 0; g < G; ++g) {
+        float M = -INFINITY, acc = 0.f, lsum = 0.f;
+        for (int64_t w = wf; w <= wl; ++w) {
+            const int64_t seg = (w + unit) * G + g;
+            const float m = a.ml_part[seg * 2];
+            const float l = a.ml_part[seg * 2 + 1];
+            const float o = a.o_part[seg * kHeadDim + d];
+            if (m == -INFINITY)
+                continue;  // a segment without valid pages
+            if (m > M) {
+                const float r = exp2f(M - m);
+                acc *= r;
+                lsum *= r;
+                M = m;
+            }
+            const float f = exp2f(m - M);
+            acc += f * o;
+            lsum += f * l;
         }
-        result = acc / lsum;
+        store_out(a.out, a.out_bf16, orow + (int64_t)g * kHeadDim, lsum > 0.f ? acc / lsum : 0.f);
     }
-    const int64_t o = (int64_t)bj * kHeadDim + d;
-    if (out_bf16)
-        static_cast<uint16_t *>(out)[o] = (uint16_t)to_bf16_bits(result);
-    else
-        static_cast<float *>(out)[o] = result;
+}
+
+// Streaming waves on the current device: compute units x resident workgroups x 4, capped.
+// (A per-process cache of device attributes; no per-call state.)
+int device_waves()
+{
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return kMaxWaves;
+    if (cached[dev] == 0) {
+        int cus = 0, per_cu = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus < 1)
+            cus = 256;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_attn_stream<true>,
+                                                         kAttnThreads, 4096) != hipSuccess ||
+            per_cu < 1)
+            per_cu = 1;
+        const int w = cus * per_cu * kAttnWaves;
+        cached[dev] = w < kMaxWaves ? w : kMaxWaves;
+    }
+    return cached[dev];
 }
 
 }  // namespace
 
-AttnPlan plan_attention(const sparrow_shape_t &s, int32_t max_count)
+AttnPlan plan_attention(const sparrow_shape_t &s)
 {
     AttnPlan p;
     const int64_t units = (int64_t)s.batch * s.num_kv_heads;
-    int pps = kTokensPerSplit / s.page_size;
-    if (pps > kMaxPagesPerSplit)
-        pps = kMaxPagesPerSplit;
-    const int min_pps = kAttnWaves;
-    if (max_count < 1)
-        max_count = 1;
-    // Small batches: shorter splits so that the grid still covers the chip.
-    while (pps > min_pps && units * ((max_count + pps - 1) / pps) < 2048)
-        pps >>= 1;
-    if (pps < min_pps)
-        pps = min_pps;
-    p.pages_per_split = pps;
-    p.max_splits = (max_count + pps - 1) / pps;
     const int G = s.num_q_heads / s.num_kv_heads;
-    const size_t per_split = (size_t)G * (kHeadDim + 2) * sizeof(float);
-    p.workspace_bytes = (size_t)units * p.max_splits * per_split;
+    p.plan_bytes = ((size_t)(s.batch + 1) * sizeof(int32_t) + 255) / 256 * 256;
+    p.segments = (size_t)kMaxWaves + (size_t)units;
+    p.workspace_bytes = p.plan_bytes + p.segments * (size_t)G * (kHeadDim + 2) * sizeof(float);
+    p.lds_bytes = (size_t)(s.batch + 1) * sizeof(int32_t);
     return p;
 }
 
@@ -311,34 +488,40 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
                             int32_t k_max, float scale, void *out, int out_dtype,
                             void *workspace, hipStream_t stream)
 {
-    const int units = s.batch * s.num_kv_heads;
     const int G = s.num_q_heads / s.num_kv_heads;
-    float *o_part = static_cast<float *>(workspace);
-    float *ml_part = o_part + (size_t)units * plan.max_splits * G * kHeadDim;
-    const float scale_log2 = scale * 1.4426950408889634f;
-    const bool sparse = idx != nullptr;
-    const dim3 grid(plan.max_splits, units);
-    if (sparse)
-        hipLaunchKernelGGL(k_attn_split<true>, grid, dim3(kAttnThreads), 0, stream,
-                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_cache),
-                           static_cast<const uint16_t *>(v_cache), block_table, seq_lens, k, idx,
-                           k_max, s.num_q_heads, s.num_kv_heads, s.page_size,
-                           s.max_pages_per_seq, plan.pages_per_split, plan.max_splits, scale_log2,
-                           o_part, ml_part);
+    AttnArgs a;
+    a.q = static_cast<const uint16_t *>(q);
+    a.k_cache = static_cast<const uint16_t *>(k_cache);
+    a.v_cache = static_cast<const uint16_t *>(v_cache);
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.ksel = k;
+    a.idx = idx;
+    a.plan_off = static_cast<int32_t *>(workspace);
+    a.o_part = reinterpret_cast<float *>(static_cast<char *>(workspace) + plan.plan_bytes);
+    a.ml_part = a.o_part + plan.segments * G * kHeadDim;
+    a.out = out;
+    a.k_max = k_max;
+    a.batch = s.batch;
+    a.num_q_heads = s.num_q_heads;
+    a.num_kv_heads = s.num_kv_heads;
+    a.ps = s.page_size;
+    a.max_pages = s.max_pages_per_seq;
+    a.out_bf16 = out_dtype == SPARROW_OUT_BF16 ? 1 : 0;
+    a.total_waves = device_waves();
+    a.scale_log2 = scale * 1.4426950408889634f;
+    const dim3 grid(a.total_waves / kAttnWaves);
+    if (idx != nullptr)
+        hipLaunchKernelGGL(k_attn_stream<true>, grid, dim3(kAttnThreads), plan.lds_bytes, stream,
+                           a);
     else
-        hipLaunchKernelGGL(k_attn_split<false>, grid, dim3(kAttnThreads), 0, stream,
-                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_cache),
-                           static_cast<const uint16_t *>(v_cache), block_table, seq_lens, nullptr,
-                           nullptr, 0, s.num_q_heads, s.num_kv_heads, s.page_size,
-                           s.max_pages_per_seq, plan.pages_per_split, plan.max_splits, scale_log2,
-                           o_part, ml_part);
+        hipLaunchKernelGGL(k_attn_stream<false>, grid, dim3(kAttnThreads), plan.lds_bytes, stream,
+                           a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_combine, dim3(s.batch * s.num_q_heads), dim3(kHeadDim), 0, stream,
-                       o_part, ml_part, seq_lens, k, k_max, sparse ? 1 : 0, s.num_q_heads,
-                       s.num_kv_heads, s.page_size, s.max_pages_per_seq, plan.pages_per_split,
-                       plan.max_splits, out, out_dtype == SPARROW_OUT_BF16 ? 1 : 0);
+    hipLaunchKernelGGL(k_attn_merge, dim3(s.batch * s.num_kv_heads), dim3(kHeadDim), 0, stream,
+                       a);
     return hipGetLastError();
 }
 

@@ -101,11 +101,13 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void
                              int32_t *out_idx, void *workspace, hipStream_t stream);
 
 struct AttnPlan {
-    int pages_per_split;
-    int max_splits;
+    size_t plan_bytes;       // per-sequence page offsets at the start of the workspace
+    size_t segments;         // partial-result slots (waves + units)
     size_t workspace_bytes;
+    size_t lds_bytes;        // dynamic LDS of the streaming kernel
 };
-AttnPlan plan_attention(const sparrow_shape_t &s, int32_t max_count);
+constexpr int kAttnMaxBatch = 8192;  // sequences per attention call (page offsets live in LDS)
+AttnPlan plan_attention(const sparrow_shape_t &s);
 hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
                             const void *k_cache, const void *v_cache, const int32_t *block_table,
                             const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
