@@ -8,8 +8,9 @@ Inputs are resident in HBM before the timed region starts.
 
 Prints ONE JSON line.  ``value`` is decode queries per second per layer
 (batch / step time).  ``roofline`` reports the dominant entry point's
-algorithmic bytes per launch over its average duration (HIP events on the
-stream the kernels are launched on) against the 8 TB/s HBM peak.
+algorithmic bytes per launch over its average duration (HIP events around K
+back-to-back launches of that entry point, on the stream its kernels run on)
+against the 8 TB/s HBM peak.
 ``cpu_baseline`` times the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -224,33 +225,37 @@ def main():
         dense_call()
     torch.cuda.synchronize()
 
-    # ---- timed sparse steps (events between the three entry points, on the same stream)
+    # ---- timed sparse steps: exactly K steps between two events, nothing else inside
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
-    for i in range(K):
-        ev[i][0].record(stream)
+    for _ in range(K):
         step.meta_update(first_pos, sp)
-        ev[i][1].record(stream)
         step.score_topk(sp)
-        ev[i][2].record(stream)
         step.attend(sp)
-        ev[i][3].record(stream)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
-    total_ms = start.elapsed_time(stop)
-    phase = {"meta_update": 0.0, "score_topk": 0.0, "sparse_attn": 0.0}
-    for e in ev:
-        phase["meta_update"] += e[0].elapsed_time(e[1])
-        phase["score_topk"] += e[1].elapsed_time(e[2])
-        phase["sparse_attn"] += e[2].elapsed_time(e[3])
-    phase = {k: v / K for k, v in phase.items()}
-    ms_step = total_ms / K
+    ms_step = start.elapsed_time(stop) / K
+
+    # ---- per-entry-point durations (a separate loop: each entry point bracketed by events
+    # on the stream its kernels run on)
+    phase = {}
+    for name, fn in (("meta_update", lambda: step.meta_update(first_pos, sp)),
+                     ("score_topk", lambda: step.score_topk(sp)),
+                     ("sparse_attn", lambda: step.attend(sp))):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(K):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        phase[name] = e0.elapsed_time(e1) / K
 
     # ---- timed dense steps
     dstart = torch.cuda.Event(enable_timing=True)
@@ -306,7 +311,7 @@ def main():
                   "bytes_per_step": int(dbytes), "achieved_GBps": round(dgbps, 1),
                   "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4)},
         "speedup_vs_dense": round(ms_dense / ms_step, 3),
-        "roofline": {"kernel": {"sparse_attn": "k_attn_split<sparse> + k_combine",
+        "roofline": {"kernel": {"sparse_attn": "k_attn_stream<sparse> + k_attn_merge",
                                 "score_topk": "k_page_score + k_topk",
                                 "meta_update": "k_meta_update"}[dominant],
                      "bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,

@@ -45,8 +45,8 @@
  *  - Supported shapes: head_dim == 128; page_size in {16, 32, 64, 128};
  *    num_q_heads a multiple of num_kv_heads with G <= 16;
  *    1 <= max_pages_per_seq <= SPARROW_MAX_PAGES_PER_SEQ;
- *    batch * num_kv_heads <= 65535; batch <= SPARROW_MAX_ATTN_BATCH for the
- *    two attention entry points.
+ *    batch * num_kv_heads <= 65535; batch <= SPARROW_MAX_BATCH for the
+ *    scoring and attention entry points.
  */
 #ifndef SPARROW_H
 #define SPARROW_H
@@ -65,7 +65,7 @@ extern "C" {
 #define SPARROW_EHIP (-4)         /* a kernel launch failed                           */
 
 #define SPARROW_MAX_PAGES_PER_SEQ 15360
-#define SPARROW_MAX_ATTN_BATCH 8192
+#define SPARROW_MAX_BATCH 8192
 
 #define SPARROW_OUT_F32 0
 #define SPARROW_OUT_BF16 1

@@ -68,6 +68,8 @@ int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const v
         return SPARROW_OK;
     if ((int64_t)shape->batch * shape->num_kv_heads > 65535)
         return SPARROW_EINVAL;
+    if (shape->batch > kMaxBatch)
+        return SPARROW_EUNSUPPORTED;
     if (!workspace || ws_bytes < score_topk_workspace(*shape))
         return SPARROW_EWORKSPACE;
     Sched sched{schedule->bin_tokens, schedule->n_bins, schedule->frac_den, schedule->min_pages,
@@ -94,7 +96,7 @@ int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, cons
         return SPARROW_EUNSUPPORTED;
     if (shape->batch == 0)
         return SPARROW_OK;
-    if (shape->batch > kAttnMaxBatch)
+    if (shape->batch > kMaxBatch)
         return SPARROW_EUNSUPPORTED;
     const AttnPlan plan = plan_attention(*shape);
     if (!workspace || ws_bytes < plan.workspace_bytes)
@@ -118,7 +120,7 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
         return SPARROW_EUNSUPPORTED;
     if (shape->batch == 0)
         return SPARROW_OK;
-    if (shape->batch > kAttnMaxBatch)
+    if (shape->batch > kMaxBatch)
         return SPARROW_EUNSUPPORTED;
     const AttnPlan plan = plan_attention(*shape);
     if (!workspace || ws_bytes < plan.workspace_bytes)
@@ -133,11 +135,11 @@ size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32
     if (check_shape(shape) != SPARROW_OK)
         return 0;
     switch (op) {
-    case SPARROW_OP_SCORE_TOPK: return score_topk_workspace(*shape);
+    case SPARROW_OP_SCORE_TOPK: return shape->batch > kMaxBatch ? 0 : score_topk_workspace(*shape);
     case SPARROW_OP_SPARSE_ATTN:
-        return k_max < 1 || shape->batch > kAttnMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
+        return k_max < 1 || shape->batch > kMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
     case SPARROW_OP_DENSE_ATTN:
-        return shape->batch > kAttnMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
+        return shape->batch > kMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
     default: return 0;
     }
 }

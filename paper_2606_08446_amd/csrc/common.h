@@ -10,6 +10,7 @@
 namespace sparrow {
 
 constexpr int kHeadDim = 128;
+constexpr int kMaxBatch = SPARROW_MAX_BATCH;  // sequences per call (page offsets live in LDS)
 
 // MFMA operand / accumulator types (wave64, 16x16 tiles).
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));  // 16x16x32 bf16 operand
@@ -106,7 +107,7 @@ struct AttnPlan {
     size_t workspace_bytes;
     size_t lds_bytes;        // dynamic LDS of the streaming kernel
 };
-constexpr int kAttnMaxBatch = 8192;  // sequences per attention call (page offsets live in LDS)
+
 AttnPlan plan_attention(const sparrow_shape_t &s);
 hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
                             const void *k_cache, const void *v_cache, const int32_t *block_table,

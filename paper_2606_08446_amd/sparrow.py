@@ -27,7 +27,7 @@ SPARROW_EUNSUPPORTED = -2
 SPARROW_EWORKSPACE = -3
 SPARROW_EHIP = -4
 SPARROW_MAX_PAGES_PER_SEQ = 15360
-SPARROW_MAX_ATTN_BATCH = 8192
+SPARROW_MAX_BATCH = 8192
 SPARROW_OUT_F32 = 0
 SPARROW_OUT_BF16 = 1
 SPARROW_OP_SCORE_TOPK = 0
