@@ -180,7 +180,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sparse decode "
-              "path has no multi-GPU mode in this build.", file=sys.stderr, flush=True)
+              "path runs one process per GPU and has no multi-GPU mode.", file=sys.stderr, flush=True)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()

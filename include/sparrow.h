@@ -28,6 +28,9 @@
  *    contents (for example a block-table entry outside [0, num_phys_pages))
  *    are the caller's contract and surface at the caller's next synchronisation.
  *  - bf16 tensors are IEEE bfloat16 bit patterns.  NaN inputs are not supported.
+ *  - Alignment: q, k_cache, v_cache, meta, out and workspace start on a 16-byte
+ *    boundary and the int32 arrays on a 4-byte boundary (any hipMalloc or PyTorch
+ *    allocation is); a misaligned pointer is rejected with SPARROW_EINVAL.
  *  - Layouts (row-major, no padding):
  *      q            bf16  [batch][num_q_heads][head_dim]
  *      k_cache      bf16  [num_phys_pages][num_kv_heads][page_size][head_dim]

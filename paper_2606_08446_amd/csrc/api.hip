@@ -28,6 +28,10 @@ int check_shape(const sparrow_shape_t *s)
     return SPARROW_OK;
 }
 
+// The kernels move bf16/fp32 data in 16-byte vectors and indices as int32.
+bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool al4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
 int status_of(hipError_t e) { return e == hipSuccess ? SPARROW_OK : SPARROW_EHIP; }
 
 }  // namespace
@@ -42,6 +46,8 @@ int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
     if (rc != SPARROW_OK)
         return rc;
     if (!k_cache || !block_table || !seq_lens || !meta)
+        return SPARROW_EINVAL;
+    if (!al16(k_cache) || !al16(meta) || !al4(block_table) || !al4(seq_lens) || !al4(first_pos))
         return SPARROW_EINVAL;
     if (shape->batch == 0)
         return SPARROW_OK;
@@ -60,6 +66,9 @@ int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const v
     if (rc != SPARROW_OK)
         return rc;
     if (!q || !meta || !block_table || !seq_lens || !schedule || !out_k || !out_idx)
+        return SPARROW_EINVAL;
+    if (!al16(q) || !al16(meta) || !al4(block_table) || !al4(seq_lens) || !al4(out_k) ||
+        !al4(out_idx) || !al16(workspace))
         return SPARROW_EINVAL;
     if (k_max < 1 || schedule->bin_tokens < 1 || schedule->n_bins < 1 || schedule->frac_den < 1 ||
         !schedule->min_pages || !schedule->frac_num)
@@ -90,6 +99,9 @@ int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, cons
         return rc;
     if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !k || !idx || !out)
         return SPARROW_EINVAL;
+    if (!al16(q) || !al16(k_cache) || !al16(v_cache) || !al4(block_table) || !al4(seq_lens) ||
+        !al4(k) || !al4(idx) || !al16(out) || !al16(workspace))
+        return SPARROW_EINVAL;
     if (k_max < 1)
         return SPARROW_EINVAL;
     if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
@@ -115,6 +127,9 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
     if (rc != SPARROW_OK)
         return rc;
     if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+        return SPARROW_EINVAL;
+    if (!al16(q) || !al16(k_cache) || !al16(v_cache) || !al4(block_table) || !al4(seq_lens) ||
+        !al16(out) || !al16(workspace))
         return SPARROW_EINVAL;
     if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
         return SPARROW_EUNSUPPORTED;

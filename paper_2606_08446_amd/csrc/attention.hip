@@ -42,7 +42,8 @@ struct AttnArgs {
     const int32_t *seq_lens;
     const int32_t *ksel;
     const int32_t *idx;
-    int32_t *plan_off;  // [batch + 1] page offsets of the sequences (written by workgroup 0)
+    int32_t *plan_off;    // [batch + 1] page offsets of the sequences (written by workgroup 0)
+    int32_t *unit_waves;  // [batch * num_kv_heads][2] first and last wave of each unit
     float *o_part;
     float *ml_part;
     void *out;
@@ -350,6 +351,12 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
             float l_tot = l_run + __shfl_xor(l_run, 16, 64);
             l_tot += __shfl_xor(l_tot, 32, 64);
             const int unit = bc.b * Hkv + bc.h;
+            if (lane == 0) {
+                if (from_start)
+                    a.unit_waves[2 * unit] = w;
+                if (bc.ends_unit)
+                    a.unit_waves[2 * unit + 1] = w;
+            }
             if (lr < G) {
                 if (from_start && bc.ends_unit) {
                     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -397,52 +404,90 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
     }
 }
 
-// Merges the partials of a (sequence, KV head) that spans several waves, and writes zero
-// rows for sequences without pages.  One 128-thread workgroup per (sequence, KV head),
-// thread = channel; one pass over the unit's segments with a running maximum.
-__global__ __launch_bounds__(kHeadDim) void k_attn_merge(AttnArgs a)
+// Merges the partials of a query-head row whose (sequence, KV head) unit spans several waves,
+// and writes zero rows for sequences without pages.  A half-wave (32 lanes, 4 channels per
+// lane) per query-head row, 8 rows per 256-thread workgroup, no LDS.  Segments are taken
+// kMergeChunk at a time: every lane issues the loads of its channels for the whole chunk at
+// once while lane t loads the (m, l) pair of segment t; the weights 2^(m - M) against the
+// running maximum M are formed with half-wave shuffles.
+constexpr int kMergeChunk = 16;
+constexpr int kMergeThreads = 256;
+constexpr int kMergeRows = kMergeThreads / 32;
+
+__device__ __forceinline__ void store_out4(void *out, int out_bf16, int64_t i, f32x4_t v)
 {
-    const int unit = blockIdx.x;
+    if (out_bf16)
+        *reinterpret_cast<u32x2_t *>(static_cast<uint16_t *>(out) + i) =
+            (u32x2_t){pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+    else
+        st16(static_cast<float *>(out) + i, __builtin_bit_cast(u32x4_t, v));
+}
+
+__global__ __launch_bounds__(kMergeThreads) void k_attn_merge(AttnArgs a)
+{
+    const int Hq = a.num_q_heads;
     const int Hkv = a.num_kv_heads;
-    const int b = unit / Hkv;
-    const int h = unit - b * Hkv;
-    const int G = a.num_q_heads / Hkv;
-    const int d = threadIdx.x;
-    const int64_t cnt = a.plan_off[b + 1] - a.plan_off[b];
-    const int64_t orow = ((int64_t)b * a.num_q_heads + (int64_t)h * G) * kHeadDim + d;
-    if (cnt == 0) {
-        for (int g = 0; g < G; ++g)
-            store_out(a.out, a.out_bf16, orow + (int64_t)g * kHeadDim, 0.f);
+    const int G = Hq / Hkv;
+    const int row = blockIdx.x * kMergeRows + (threadIdx.x >> 5);
+    if (row >= a.batch * Hq)
+        return;
+    const int t = threadIdx.x & 31;  // lane within the half-wave
+    const int b = row / Hq;
+    const int j = row - b * Hq;
+    const int h = j / G;
+    const int g = j - h * G;
+    const int unit = b * Hkv + h;
+    const int64_t orow = (int64_t)row * kHeadDim + 4 * t;
+    const int32_t o0 = a.plan_off[b], o1 = a.plan_off[b + 1];
+    const int wf = a.unit_waves[2 * unit];      // wave holding the unit's first page
+    const int wl = a.unit_waves[2 * unit + 1];  // wave holding its last page
+    if (o1 == o0) {
+        store_out4(a.out, a.out_bf16, orow, (f32x4_t){0.f, 0.f, 0.f, 0.f});
         return;
     }
-    const int64_t P = (int64_t)a.plan_off[a.batch] * Hkv;
-    const int64_t W = P < a.total_waves ? P : a.total_waves;
-    const int64_t off = (int64_t)a.plan_off[b] * Hkv + h * cnt;
-    const int64_t wf = ((off + 1) * W - 1) / P;    // wave holding the unit's first page
-    const int64_t wl = ((off + cnt) * W - 1) / P;  // wave holding its last page
     if (wf == wl)
         return;  // one wave held the whole unit and wrote its output
-    for (int g = 0; g < G; ++g) {
-        float M = -INFINITY, acc = 0.f, lsum = 0.f;
-        for (int64_t w = wf; w <= wl; ++w) {
-            const int64_t seg = (w + unit) * G + g;
-            const float m = a.ml_part[seg * 2];
-            const float l = a.ml_part[seg * 2 + 1];
-            const float o = a.o_part[seg * kHeadDim + d];
-            if (m == -INFINITY)
-                continue;  // a segment without valid pages
-            if (m > M) {
-                const float r = exp2f(M - m);
-                acc *= r;
-                lsum *= r;
-                M = m;
-            }
-            const float f = exp2f(m - M);
-            acc += f * o;
-            lsum += f * l;
+    const int nseg = wl - wf + 1;
+    const int64_t seg0 = (int64_t)wf + unit;  // segment of wave wf for this unit
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    float M = -INFINITY, lsum = 0.f;
+    for (int c0 = 0; c0 < nseg; c0 += kMergeChunk) {
+        const int n = nseg - c0 < kMergeChunk ? nseg - c0 : kMergeChunk;
+        f32x4_t o[kMergeChunk];
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i) {
+            o[i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+            if (i < n)
+                o[i] = __builtin_bit_cast(
+                    f32x4_t, ld16(a.o_part + ((seg0 + c0 + i) * G + g) * kHeadDim + 4 * t));
         }
-        store_out(a.out, a.out_bf16, orow + (int64_t)g * kHeadDim, lsum > 0.f ? acc / lsum : 0.f);
+        float m = -INFINITY, l = 0.f;
+        if (t < n) {
+            const int64_t sg = (seg0 + c0 + t) * G + g;
+            m = a.ml_part[sg * 2];
+            l = a.ml_part[sg * 2 + 1];
+        }
+        float cm = m;
+#pragma unroll
+        for (int x = 1; x < 32; x <<= 1)
+            cm = fmaxf(cm, __shfl_xor(cm, x, 64));
+        const float Mn = fmaxf(M, cm);
+        const float r = M == -INFINITY ? 0.f : exp2f(M - Mn);
+        const float f = m == -INFINITY ? 0.f : exp2f(m - Mn);  // no valid pages: weight 0
+        float fl = f * l;
+#pragma unroll
+        for (int x = 1; x < 32; x <<= 1)
+            fl += __shfl_xor(fl, x, 64);
+        lsum = lsum * r + fl;
+        M = Mn;
+        acc *= r;
+        const int base = threadIdx.x & 32;  // first lane of this half-wave
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i)
+            acc += __shfl(f, base + i, 64) * o[i];
     }
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+    store_out4(a.out, a.out_bf16, orow, acc * inv);
 }
 
 // Streaming waves on the current device: compute units x resident workgroups x 4, capped.
@@ -475,7 +520,8 @@ AttnPlan plan_attention(const sparrow_shape_t &s)
     AttnPlan p;
     const int64_t units = (int64_t)s.batch * s.num_kv_heads;
     const int G = s.num_q_heads / s.num_kv_heads;
-    p.plan_bytes = ((size_t)(s.batch + 1) * sizeof(int32_t) + 255) / 256 * 256;
+    p.plan_bytes = ((size_t)(s.batch + 1) * sizeof(int32_t) + 255) / 256 * 256 +
+                   ((size_t)units * 2 * sizeof(int32_t) + 255) / 256 * 256;
     p.segments = (size_t)kMaxWaves + (size_t)units;
     p.workspace_bytes = p.plan_bytes + p.segments * (size_t)G * (kHeadDim + 2) * sizeof(float);
     p.lds_bytes = (size_t)(s.batch + 1) * sizeof(int32_t);
@@ -498,6 +544,7 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     a.ksel = k;
     a.idx = idx;
     a.plan_off = static_cast<int32_t *>(workspace);
+    a.unit_waves = a.plan_off + ((size_t)(s.batch + 1) + 63) / 64 * 64;
     a.o_part = reinterpret_cast<float *>(static_cast<char *>(workspace) + plan.plan_bytes);
     a.ml_part = a.o_part + plan.segments * G * kHeadDim;
     a.out = out;
@@ -520,8 +567,9 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_attn_merge, dim3(s.batch * s.num_kv_heads), dim3(kHeadDim), 0, stream,
-                       a);
+    const int rows = s.batch * s.num_q_heads;
+    hipLaunchKernelGGL(k_attn_merge, dim3((rows + kMergeRows - 1) / kMergeRows),
+                       dim3(kMergeThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -102,7 +102,7 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void
                              int32_t *out_idx, void *workspace, hipStream_t stream);
 
 struct AttnPlan {
-    size_t plan_bytes;       // per-sequence page offsets at the start of the workspace
+    size_t plan_bytes;       // page offsets and unit wave ranges at the start of the workspace
     size_t segments;         // partial-result slots (waves + units)
     size_t workspace_bytes;
     size_t lds_bytes;        // dynamic LDS of the streaming kernel

@@ -188,3 +188,20 @@ def test_tensor_wrappers_refuse_host_tensors():
         S.dense_decode_attn(q, torch.zeros(2, 1, 16, 128, dtype=torch.bfloat16),
                             torch.zeros(2, 1, 16, 128, dtype=torch.bfloat16),
                             torch.zeros(1, 2, dtype=torch.int32), torch.ones(1, dtype=torch.int32))
+
+
+VEC16 = {"meta": ["k_cache", "meta"], "topk": ["q", "meta", "ws"],
+         "sparse": ["q", "k", "v", "out", "ws"], "dense": ["q", "k", "v", "out", "ws"]}
+
+
+@pytest.mark.parametrize("fn,arg", [(f, a) for f, args in NULLS.items() for a in args] +
+                         [(f, a) for f, args in VEC16.items() for a in args if a == "ws"] +
+                         [("meta", "first_pos")])
+def test_misaligned_pointers_are_rejected(lib, fn, arg):
+    # Every pointer the kernels read or write must be at least 4-byte aligned.
+    assert call(fn, good_shape(), **{arg: FAKE + 2}) == S.SPARROW_EINVAL
+
+
+@pytest.mark.parametrize("fn,arg", [(f, a) for f, args in VEC16.items() for a in args])
+def test_vector_pointers_need_16_byte_alignment(lib, fn, arg):
+    assert call(fn, good_shape(), **{arg: FAKE + 4}) == S.SPARROW_EINVAL
