@@ -28,7 +28,7 @@ if ROOT not in sys.path:
 
 METRIC = "sparse decode attn queries/sec per layer + achieved HBM GB/s (% of peak) vs dense"
 HBM_PEAK_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_attn.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_attn_c2_qwen3_1p7b_b64.txt")
 
 
 def parse():
@@ -87,8 +87,9 @@ def dense_bytes(inp):
         len(inp.lens_host) * w.num_q_heads * 128 * (2 + 4)
 
 
-def read_traffic(kernel_src_sha):
-    """HBM traffic per launch from the committed counter summary, if it matches the source."""
+def read_traffic(kernel_src_sha, workload_name):
+    """HBM traffic per launch from the committed counter summary, if it was taken on this
+    workload with the current attention source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     vals = {}
@@ -96,7 +97,8 @@ def read_traffic(kernel_src_sha):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("source_sha256") != kernel_src_sha or "traffic_bytes_per_launch" not in vals:
+    if vals.get("source_sha256") != kernel_src_sha or vals.get("workload") != workload_name or \
+            "traffic_bytes_per_launch" not in vals:
         return None
     return float(vals["traffic_bytes_per_launch"])
 
@@ -278,7 +280,7 @@ def main():
     dgbps = dbytes / (ms_dense * 1e-3) / 1e9
     dominant = max(phase, key=phase.get)
     dom_gbps = by[dominant] / (phase[dominant] * 1e-3) / 1e9
-    traffic = read_traffic(source_sha()) if dominant == "sparse_attn" else None
+    traffic = read_traffic(source_sha(), w.name) if dominant == "sparse_attn" else None
 
     cpu = None
     if not args.no_cpu_baseline:
