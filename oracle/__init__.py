@@ -38,6 +38,8 @@ def _load():
     lib.oracle_budgets.restype = None
     lib.oracle_page_meta.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p]
     lib.oracle_page_meta.restype = None
+    lib.oracle_append_kv.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p]
+    lib.oracle_append_kv.restype = None
     lib.oracle_page_scores.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p,
                                        _p, _p]
     lib.oracle_page_scores.restype = None
@@ -101,6 +103,23 @@ def page_meta(k_cache, block_table, seq_lens, first_pos=None, meta=None) -> np.n
     fp_arr, fpp = (None, None) if first_pos is None else _c(first_pos, np.int32)
     _load().oracle_page_meta(B, Hkv, D, ps, max_pages, kcp, btp, slp, fpp, out.ctypes.data)
     return out
+
+
+def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta):
+    """Copies of (k_cache, v_cache, meta) after writing token ``L_b - 1`` of every sequence
+    (rows ``k_new``/``v_new`` ``[B][Hkv][D]``) and rebuilding the metadata of its page."""
+    P, Hkv, ps, D = k_cache.shape
+    B, max_pages = block_table.shape
+    kn, knp = _c(k_new, np.uint16)
+    vn, vnp = _c(v_new, np.uint16)
+    kc = np.array(k_cache, dtype=np.uint16, copy=True, order="C")
+    vc = np.array(v_cache, dtype=np.uint16, copy=True, order="C")
+    mt = np.array(meta, dtype=np.uint16, copy=True, order="C")
+    bt, btp = _c(block_table, np.int32)
+    sl, slp = _c(seq_lens, np.int32)
+    _load().oracle_append_kv(B, Hkv, D, ps, max_pages, knp, vnp, kc.ctypes.data, vc.ctypes.data,
+                             btp, slp, mt.ctypes.data)
+    return kc, vc, mt
 
 
 def page_scores(q, meta, block_table, seq_lens, ps):

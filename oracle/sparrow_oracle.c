@@ -159,6 +159,43 @@ void oracle_page_meta(int32_t B, int32_t Hkv, int32_t D, int32_t ps, int32_t max
 }
 
 /* ------------------------------------------------------------------------ */
+/* Appending the token being decoded (the step that precedes scoring in a    */
+/* decode step; Sec. 3.3 counts the landmark upkeep per generated token).    */
+/* L_b counts the new token, so it sits at position L_b - 1: logical page    */
+/* (L_b - 1) / ps, slot (L_b - 1) % ps.  Its key and value rows of every KV  */
+/* head are copied into the caches, then the metadata of that page is        */
+/* recomputed from all of its valid tokens (the definition above).           */
+/* Sequences with L_b < 1, or with L_b beyond what the block table can       */
+/* address, are left untouched.  New rows: k_new, v_new bf16 [B][Hkv][D].    */
+/* ------------------------------------------------------------------------ */
+void oracle_append_kv(int32_t B, int32_t Hkv, int32_t D, int32_t ps, int32_t max_pages,
+                      const uint16_t *k_new, const uint16_t *v_new, uint16_t *k_cache,
+                      uint16_t *v_cache, const int32_t *block_table, const int32_t *seq_lens,
+                      uint16_t *meta)
+{
+    for (int32_t b = 0; b < B; ++b) {
+        int64_t L = seq_lens[b];
+        if (L < 1 || L > (int64_t)ps * max_pages)
+            continue;
+        int64_t pos = L - 1;
+        int64_t phys = block_table[(int64_t)b * max_pages + pos / ps];
+        int64_t slot = pos % ps;
+        for (int32_t h = 0; h < Hkv; ++h) {
+            int64_t row = ((phys * Hkv + h) * ps + slot) * D;
+            const uint16_t *kn = k_new + ((int64_t)b * Hkv + h) * D;
+            const uint16_t *vn = v_new + ((int64_t)b * Hkv + h) * D;
+            for (int32_t i = 0; i < D; ++i) {
+                k_cache[row + i] = kn[i];
+                v_cache[row + i] = vn[i];
+            }
+        }
+        int32_t first = (int32_t)pos;
+        oracle_page_meta(1, Hkv, D, ps, max_pages, k_cache, block_table + (int64_t)b * max_pages,
+                         seq_lens + b, &first, meta);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
 /* Page scores.  s_j(p) = sum_i max(q_{j,i} mn_i, q_{j,i} mx_i) is an upper  */
 /* bound of q_j . k_t over the tokens t of page p; the KV-head score is the  */
 /* sum of s_j over its G query heads.  scores32 is accumulated in fp32,      */

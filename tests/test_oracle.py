@@ -112,6 +112,76 @@ def test_meta_incremental_update_equals_rebuild(step):
             np.testing.assert_array_equal(updated[d["bt"][b, p]], rebuilt[d["bt"][b, p]])
 
 
+# ----------------------------------------------------------------------------- append
+def _rand_bits(rng, shape):
+    return f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32))
+
+
+def test_append_writes_exactly_one_row_per_head_and_rebuilds_its_page():
+    # lengths: mid-page, first slot of a fresh page, last slot of a page, empty, beyond the table
+    d = host_inputs(B=5, lengths=(37, 33, 48, 0, 20), seed=21)
+    rng = np.random.default_rng(5)
+    B, Hkv, D, ps = 5, 2, 128, 16
+    lens = d["lens"].copy()
+    cap = ps * d["bt"].shape[1]
+    lens[4] = cap + 1                       # cannot be addressed: skipped
+    kn, vn = _rand_bits(rng, (B, Hkv, D)), _rand_bits(rng, (B, Hkv, D))
+    meta0 = oracle.page_meta(d["k"], d["bt"], np.minimum(lens, cap).astype(np.int32))
+    kc, vc, mt = oracle.append_kv(kn, vn, d["k"], d["v"], d["bt"], lens, meta0)
+    k_exp, v_exp = d["k"].copy(), d["v"].copy()
+    touched = []
+    for b, L in enumerate(lens):
+        if L < 1 or L > cap:
+            continue
+        phys, slot = d["bt"][b, (L - 1) // ps], (L - 1) % ps
+        k_exp[phys, :, slot], v_exp[phys, :, slot] = kn[b], vn[b]
+        touched.append((b, phys, min(ps, L - (L - 1) // ps * ps)))
+    np.testing.assert_array_equal(kc, k_exp)        # the new rows and nothing else
+    np.testing.assert_array_equal(vc, v_exp)
+    for b, phys, valid in touched:
+        for h in range(Hkv):
+            rows = k_exp[phys, h, :valid]
+            keys = order_key(rows)
+            np.testing.assert_array_equal(mt[phys, h, 0],
+                                          rows[np.argmin(keys, 0), np.arange(D)])
+            np.testing.assert_array_equal(mt[phys, h, 1],
+                                          rows[np.argmax(keys, 0), np.arange(D)])
+    # pages nobody appended to keep their metadata
+    untouched = np.ones(mt.shape[0], bool)
+    untouched[[t[1] for t in touched]] = False
+    np.testing.assert_array_equal(mt[untouched], meta0[untouched])
+
+
+def test_appending_token_by_token_equals_building_at_once():
+    # Grow three sequences from empty, one token per step, and compare with writing the
+    # whole sequences into the cache first and building the metadata in one pass.
+    d = host_inputs(B=3, lengths=(40, 16, 17), seed=22)
+    full = d["lens"].copy()
+    B, Hkv = 3, 2
+    kc = np.zeros_like(d["k"])
+    vc = np.zeros_like(d["v"])
+    mt = np.zeros((kc.shape[0], Hkv, 2, 128), np.uint16)
+    for t in range(int(full.max())):
+        lens = np.minimum(full, t + 1).astype(np.int32)
+        grow = (full > t)
+        kn = np.zeros((B, Hkv, 128), np.uint16)
+        vn = np.zeros((B, Hkv, 128), np.uint16)
+        for b in range(B):
+            if grow[b]:
+                phys = d["bt"][b, t // 16]
+                kn[b], vn[b] = d["k"][phys, :, t % 16], d["v"][phys, :, t % 16]
+        lens_step = np.where(grow, lens, 0).astype(np.int32)   # finished sequences sit out
+        kc, vc, mt = oracle.append_kv(kn, vn, kc, vc, d["bt"], lens_step, mt)
+    rebuilt = oracle.page_meta(d["k"], d["bt"], full)
+    for b, L in enumerate(full):
+        for p in range((L + 15) // 16):
+            phys = d["bt"][b, p]
+            valid = min(16, L - p * 16)
+            np.testing.assert_array_equal(kc[phys, :, :valid], d["k"][phys, :, :valid])
+            np.testing.assert_array_equal(vc[phys, :, :valid], d["v"][phys, :, :valid])
+            np.testing.assert_array_equal(mt[phys], rebuilt[phys])
+
+
 # ----------------------------------------------------------------------------- scores
 def brute_scores64(d, meta, b, h, G):
     n = (int(d["lens"][b]) + d["ps"] - 1) // d["ps"]

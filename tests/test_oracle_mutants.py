@@ -40,6 +40,9 @@ MUTANTS = {
     "budget_no_page_clamp": ("    if (k > n)\n        k = n;\n    return (int32_t)k;",
                              "    return (int32_t)k;"),
     "select_pads_with_zero": ("row[i] = -1;", "row[i] = 0;"),
+    "append_to_next_slot": ("int64_t pos = L - 1;", "int64_t pos = L;"),
+    "append_skips_meta_rebuild": ("        int32_t first = (int32_t)pos;\n        oracle_page_meta(",
+                                  "        int32_t first = (int32_t)L;\n        oracle_page_meta("),
 }
 
 
