@@ -1,10 +1,12 @@
 """Benchmark of the sparse decode step on one MI355X.
 
-One step = one decode step of one attention layer for the whole batch:
-metadata update of the page holding each sequence's newest token, page
-scoring + budget + top-k, sparse attention over the selected pages (split-KV
-and combine).  The dense paged decode over the same cache is timed beside it.
-Inputs are resident in HBM before the timed region starts.
+One step = one decode step of one attention layer for the whole batch: append
+the new token's K/V to the paged cache with its page's metadata, page scoring
++ budget + top-k (fused with the append by default), sparse attention over the
+selected pages.  Every step appends one token per sequence, so the lengths
+advance by one per step.  The dense decode (append + attention over every
+token) is timed beside it on the same steps.  Inputs are resident in HBM
+before the timed region starts.
 
 Prints ONE JSON line.  ``value`` is decode queries per second per layer
 (batch / step time).  ``roofline`` reports the dominant entry point's
@@ -40,6 +42,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--step", choices=("fused", "separate"), default="fused",
+                    help="fused: sparrow_append_score_topk + attention; separate: "
+                         "sparrow_append_kv, sparrow_page_score_topk, attention")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for counter scaling)")
     return ap.parse_args()
@@ -53,13 +58,12 @@ def workload(name):
     return W.CONFIGS[name]
 
 
-def sparse_bytes(inp, k_host, idx_host):
-    """Algorithmic HBM bytes of one sparse step, per phase."""
-    import numpy as np
+def sparse_bytes(inp, lens, k_host, idx_host):
+    """Algorithmic HBM bytes of one sparse decode step at lengths ``lens`` (the appended
+    token included), per entry point."""
     w = inp.workload
     ps, Hkv, Hq, D = w.page_size, w.num_kv_heads, w.num_q_heads, 128
-    lens = inp.lens_host
-    meta_update = 0
+    append = 0
     score = 0
     kv = 0
     for b, L in enumerate(lens):
@@ -68,7 +72,9 @@ def sparse_bytes(inp, k_host, idx_host):
             continue
         n = -(-L // ps)
         last_valid = L - (n - 1) * ps
-        meta_update += Hkv * (last_valid * D * 2 + 2 * D * 2)       # read page keys, write meta
+        # new K and V rows read and written; the page's metadata read (unless the token
+        # opens the page) and written
+        append += Hkv * (2 * (2 * D * 2) + (2 * D * 2 if last_valid > 1 else 0) + 2 * D * 2)
         k = int(k_host[b])
         if k < n:
             score += Hkv * n * 2 * D * 2                              # meta rows
@@ -77,14 +83,16 @@ def sparse_bytes(inp, k_host, idx_host):
             toks = k * ps - (ps - last_valid if (n - 1) in set(sel.tolist()) else 0)
             kv += toks * 2 * D * 2                                    # K and V rows
     q_out = len(lens) * Hq * D * (2 + 4)
-    return {"meta_update": meta_update, "score_topk": score + len(lens) * Hq * D * 2,
+    return {"append": append, "score_topk": score + len(lens) * Hq * D * 2,
             "sparse_attn": kv + q_out}
 
 
-def dense_bytes(inp):
+def dense_bytes(inp, lens):
+    """Algorithmic bytes of the dense step: the append's K/V rows and every valid K/V row."""
     w = inp.workload
-    return int(sum(int(L) for L in inp.lens_host)) * w.num_kv_heads * 2 * 128 * 2 + \
-        len(inp.lens_host) * w.num_q_heads * 128 * (2 + 4)
+    B = len(lens)
+    return int(sum(int(L) for L in lens)) * w.num_kv_heads * 2 * 128 * 2 + \
+        B * w.num_q_heads * 128 * (2 + 4) + B * w.num_kv_heads * 4 * 128 * 2
 
 
 def read_traffic(kernel_src_sha, workload_name):
@@ -112,8 +120,10 @@ def source_sha():
     return h.hexdigest()
 
 
-def cpu_baseline(inp, k_max, target_s):
-    """The oracle's sparse step on a sample of sequences, repeated to ~target_s seconds."""
+def cpu_baseline(inp, lens_step, k_new, v_new, k_max, target_s):
+    """The oracle's sparse decode step on a sample of sequences, repeated to ~target_s
+    seconds: append the new token, rebuild its page's metadata, score, budget, top-k,
+    attention.  ``lens_step`` are the lengths of the step (the new token included)."""
     import numpy as np
     import torch
 
@@ -125,30 +135,32 @@ def cpu_baseline(inp, k_max, target_s):
     B = w.batch
     n_seq = min(B, 8)
     seqs = list(range(n_seq))
+    lens = np.asarray(lens_step[:n_seq], np.int32)
     bt_all = inp.block_table.cpu().numpy()
     phys, rows = [], []
-    for b in seqs:
-        n = -(-int(inp.lens_host[b]) // ps)
+    for i, b in enumerate(seqs):
+        n = -(-int(lens[i]) // ps)
         rows.append(len(phys))
         phys.extend(int(x) for x in bt_all[b, :n])
-    max_n = max(1, max(-(-int(inp.lens_host[b]) // ps) for b in seqs))
+    max_n = max(1, max(-(-int(L) // ps) for L in lens))
     bt = np.zeros((n_seq, max_n), np.int32)
-    for i, b in enumerate(seqs):
-        n = -(-int(inp.lens_host[b]) // ps)
+    for i in range(n_seq):
+        n = -(-int(lens[i]) // ps)
         bt[i, :n] = np.arange(rows[i], rows[i] + n)
     pi = torch.as_tensor(np.array(phys, np.int64), device=inp.k_cache.device)
     q = W.bf16_bits(inp.q[:n_seq])
     kc = W.bf16_bits(inp.k_cache[pi])
     vc = W.bf16_bits(inp.v_cache[pi])
-    lens = inp.lens_host[:n_seq].astype(np.int32)
-    meta = oracle.page_meta(kc, bt, lens)       # setup: metadata before the step
-    first = (lens - 1).astype(np.int32)
+    kn = W.bf16_bits(k_new[:n_seq])
+    vn = W.bf16_bits(v_new[:n_seq])
+    meta = oracle.page_meta(kc, bt, (lens - 1).astype(np.int32))  # setup: before the step
     scale = 1.0 / math.sqrt(128.0)
     reps = 0
     t0 = time.perf_counter()
     while True:
-        m2 = oracle.page_meta(kc, bt, lens, first_pos=first, meta=meta)
-        s32, _ = oracle.page_scores(q, m2, bt, lens, ps)
+        # in place: re-appending the same token leaves the arrays as they were after the first
+        oracle.append_kv(kn, vn, kc, vc, bt, lens, meta, inplace=True)
+        s32, _ = oracle.page_scores(q, meta, bt, lens, ps)
         k = np.minimum(oracle.budgets(lens, ps, s.bin_tokens, s.min_pages, s.frac_num,
                                       s.frac_den), k_max).astype(np.int32)
         idx = oracle.select(lens, k, s32, ps, k_max)
@@ -159,9 +171,9 @@ def cpu_baseline(inp, k_max, target_s):
             break
     return {"value": round(n_seq * reps / el, 3), "unit": "queries/s",
             "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"first {n_seq} of {B} sequences of {w.name}, whole sparse step "
-                      f"(metadata update of the newest page, fp32+fp64 scores, budget, top-k, "
-                      f"fp64 attention) repeated {reps}x in {el:.1f} s"}
+            "sample": f"first {n_seq} of {B} sequences of {w.name}, whole sparse decode step "
+                      f"(append of the new token with its page's metadata rebuilt, fp32+fp64 "
+                      f"scores, budget, top-k, fp64 attention) repeated {reps}x in {el:.1f} s"}
 
 
 def copy_calibration():
@@ -188,6 +200,8 @@ def main():
         copy_calibration()
         return
 
+    import dataclasses
+
     import numpy as np
     import torch
 
@@ -196,86 +210,99 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    K, Wm = args.steps, args.warmup
     w = workload(args.workload)
+    ps = w.page_size
+    # every step appends one token per sequence: spare pages for all of them
+    w = dataclasses.replace(w, extra_pages=(Wm + K + 1 + ps - 1) // ps + 1)
     inp = W.generate(w, dev)
     s = w.schedule
-    k_max = S.budget_bound(inp.lens_host, w.page_size, s.bin_tokens, s.min_pages, s.frac_num,
+    B, Hkv = w.batch, w.num_kv_heads
+    total = Wm + K
+    # step i appends the token at position lens0 + i: its lengths are lens0 + i + 1
+    lens0 = inp.seq_lens.clone()
+    lens_steps = (lens0[None, :] + torch.arange(1, total + 1, device=dev,
+                                                dtype=torch.int32)[:, None]).contiguous()
+    lens_host_steps = inp.lens_host[None, :] + np.arange(1, total + 1)[:, None]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 1)
+    k_new = torch.randn((total, B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
+    v_new = torch.randn((total, B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
+    k_max = S.budget_bound(lens_host_steps.ravel(), ps, s.bin_tokens, s.min_pages, s.frac_num,
                            s.frac_den)
-    meta = torch.zeros((inp.num_phys_pages, w.num_kv_heads, 2, 128), dtype=torch.bfloat16,
-                       device=dev)
-    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta)
-    step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+    meta = torch.zeros((inp.num_phys_pages, Hkv, 2, 128), dtype=torch.bfloat16, device=dev)
+    S.page_meta_update(inp.k_cache, inp.block_table, lens0, meta)
+    step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table, lens0,
                               meta, inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, k_max)
-    first_pos = (inp.seq_lens - 1).clamp(min=0)
     dense_out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
     dense_ws = torch.empty(max(16, S.sparrow_workspace_size(step.shape, 0,
                                                             S.SPARROW_OP_DENSE_ATTN)),
                            dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     sp = stream.cuda_stream
+    fused = args.step == "fused"
 
-    def dense_call():
+    def select(i):
+        if fused:
+            step.append_score_topk(k_new[i], v_new[i], sp, seq_lens=lens_steps[i])
+        else:
+            step.append(k_new[i], v_new[i], sp, seq_lens=lens_steps[i])
+            step.score_topk(sp, seq_lens=lens_steps[i])
+
+    def sparse_step(i):
+        select(i)
+        step.attend(sp, seq_lens=lens_steps[i])
+
+    def dense_step(i):
+        step.append(k_new[i], v_new[i], sp, seq_lens=lens_steps[i])
         S._check("sparrow_dense_decode_attn", S.sparrow_dense_decode_attn(
             step.shape, inp.q.data_ptr(), inp.k_cache.data_ptr(), inp.v_cache.data_ptr(),
-            inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), step.scale,
+            inp.block_table.data_ptr(), lens_steps[i].data_ptr(), step.scale,
             dense_out.data_ptr(), S.SPARROW_OUT_F32, dense_ws.data_ptr(), dense_ws.numel(), sp))
 
-    for _ in range(args.warmup):
-        step.meta_update(first_pos, sp)
-        step.score_topk(sp)
-        step.attend(sp)
-        dense_call()
-    torch.cuda.synchronize()
-
-    # ---- timed sparse steps: exactly K steps between two events, nothing else inside
-    K = args.steps
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record(stream)
-    for _ in range(K):
-        step.meta_update(first_pos, sp)
-        step.score_topk(sp)
-        step.attend(sp)
-    stop.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall
-    ms_step = start.elapsed_time(stop) / K
-
-    # ---- per-entry-point durations (a separate loop: each entry point bracketed by events
-    # on the stream its kernels run on)
-    phase = {}
-    for name, fn in (("meta_update", lambda: step.meta_update(first_pos, sp)),
-                     ("score_topk", lambda: step.score_topk(sp)),
-                     ("sparse_attn", lambda: step.attend(sp))):
+    def timed(fn, first, count):
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(stream)
-        for _ in range(K):
-            fn()
+        for i in range(first, first + count):
+            fn(i)
         e1.record(stream)
         torch.cuda.synchronize()
-        phase[name] = e0.elapsed_time(e1) / K
+        return e0.elapsed_time(e1) / count
 
-    # ---- timed dense steps
-    dstart = torch.cuda.Event(enable_timing=True)
-    dstop = torch.cuda.Event(enable_timing=True)
+    for i in range(Wm):
+        sparse_step(i)
     torch.cuda.synchronize()
-    dstart.record(stream)
-    for _ in range(K):
-        dense_call()
-    dstop.record(stream)
-    torch.cuda.synchronize()
-    ms_dense = dstart.elapsed_time(dstop) / K
 
+    # ---- timed sparse steps: exactly K steps between two events, nothing else inside
+    t_wall = time.perf_counter()
+    ms_step = timed(sparse_step, Wm, K)
+    wall = time.perf_counter() - t_wall
     k_host = step.k.cpu().numpy()
     idx_host = step.idx.cpu().numpy()
-    by = sparse_bytes(inp, k_host, idx_host)
+
+    # ---- per-entry-point durations (a separate loop over the same steps; re-running a step
+    # rewrites the same token, which leaves caches and metadata unchanged)
+    phase = {}
+    if fused:
+        phase["append_score_topk"] = timed(select, Wm, K)
+    else:
+        phase["append"] = timed(lambda i: step.append(k_new[i], v_new[i], sp,
+                                                      seq_lens=lens_steps[i]), Wm, K)
+        phase["score_topk"] = timed(lambda i: step.score_topk(sp, seq_lens=lens_steps[i]), Wm, K)
+    phase["sparse_attn"] = timed(lambda i: step.attend(sp, seq_lens=lens_steps[i]), Wm, K)
+
+    # ---- timed dense steps over the same appended tokens
+    ms_dense = timed(dense_step, Wm, K)
+
+    lens_last = lens_host_steps[-1]
+    by = sparse_bytes(inp, lens_last, k_host, idx_host)
+    if fused:
+        by = {"append_score_topk": by["append"] + by["score_topk"],
+              "sparse_attn": by["sparse_attn"]}
     total_bytes = sum(by.values())
-    dbytes = dense_bytes(inp)
-    B = w.batch
+    dbytes = dense_bytes(inp, lens_last)
     gbps = total_bytes / (ms_step * 1e-3) / 1e9
     dgbps = dbytes / (ms_dense * 1e-3) / 1e9
     dominant = max(phase, key=phase.get)
@@ -284,16 +311,19 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(inp, k_max, args.cpu_seconds)
+        cpu = cpu_baseline(inp, lens_last, k_new[-1], v_new[-1], k_max, args.cpu_seconds)
 
     budgets = np.asarray(k_host)
+    kernels = {"sparse_attn": "k_attn_stream<sparse> + k_attn_merge",
+               "append_score_topk": "k_page_score (with append) + k_topk",
+               "score_topk": "k_page_score + k_topk", "append": "k_append_kv"}
     result = {
         "metric": METRIC,
         "value": round(B / (ms_step * 1e-3), 2),
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
+        "warmup": Wm,
         "ms_per_step": round(ms_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -301,21 +331,23 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "batch": B, "num_q_heads": w.num_q_heads,
-                   "num_kv_heads": w.num_kv_heads, "head_dim": 128, "page_size": w.page_size,
+                   "num_kv_heads": Hkv, "head_dim": 128, "page_size": ps,
                    "len_range": [w.len_lo, w.len_hi], "budget_pages": [int(budgets.min()),
                                                                        int(budgets.max())],
-                   "k_max": int(k_max)},
+                   "k_max": int(k_max),
+                   "step": ("append+score+top-k fused, attention" if fused else
+                            "append, score+top-k, attention") +
+                           "; one token appended per sequence per step"},
         "achieved_GBps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": {k: int(v) for k, v in by.items()},
         "phase_ms": {k: round(v, 5) for k, v in phase.items()},
         "dense": {"queries_per_s": round(B / (ms_dense * 1e-3), 2), "ms_per_step": round(ms_dense, 5),
                   "bytes_per_step": int(dbytes), "achieved_GBps": round(dgbps, 1),
-                  "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4)},
+                  "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4),
+                  "step": "append, dense attention"},
         "speedup_vs_dense": round(ms_dense / ms_step, 3),
-        "roofline": {"kernel": {"sparse_attn": "k_attn_stream<sparse> + k_attn_merge",
-                                "score_topk": "k_page_score + k_topk",
-                                "meta_update": "k_meta_update"}[dominant],
+        "roofline": {"kernel": kernels[dominant],
                      "bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": traffic},

@@ -6,6 +6,8 @@
  *
  *   1. sparrow_page_meta_update   per-page key min/max metadata (the page
  *                                 landmark scored in Sec. 3.3 / Appendix C),
+ *                                 or sparrow_append_kv: write the decoded token's
+ *                                 K/V and update its page's metadata in O(1),
  *   2. sparrow_page_score_topk    page scores against the current query, the
  *                                 per-sequence page budget from the dynamic
  *                                 sparsity schedule (Sec. 3.2 Method box) and
@@ -16,6 +18,7 @@
  *                                 cost model, Eq. sparse-cost),
  *   4. sparrow_dense_decode_attn  the dense paged decode it is measured against
  *                                 (Eq. dense-cost).
+ *   sparrow_append_score_topk fuses the append into step 2.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -135,6 +138,30 @@ int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
                              const int32_t *first_pos, void *meta, void *stream);
 
 /*
+ * Appending the token being decoded (the per-token landmark upkeep of Sec. 3.3:
+ * the page metadata follows every generated key).
+ *
+ * seq_lens[b] counts the new token, which goes to position L - 1 = seq_lens[b] - 1:
+ * logical page (L - 1) / page_size, slot (L - 1) % page_size.  For every KV head h:
+ *     k_cache[phys][h][slot][:] = k_new[b][h][:],  v_cache[phys][h][slot][:] = v_new[b][h][:]
+ * with phys = block_table[b][(L - 1) / page_size], and the page's metadata becomes the
+ * channel-wise min/max of its old metadata and the new key (the key itself when the
+ * slot is 0).  This equals the metadata rebuilt from the page's L - page*page_size valid
+ * tokens (sparrow_page_meta_update) provided the old metadata described the tokens
+ * before L - 1.  Sequences with seq_lens[b] < 1 or seq_lens[b] > max_pages_per_seq *
+ * page_size are left untouched.  Sequences must use distinct physical pages.
+ *
+ * Arguments: shape (host); k_new, v_new (device bf16 [batch][num_kv_heads][head_dim]);
+ * k_cache, v_cache, meta (device, updated in place); block_table, seq_lens (device);
+ * stream.
+ * Errors: SPARROW_EINVAL (null or misaligned pointer, bad size), SPARROW_EUNSUPPORTED,
+ * SPARROW_EHIP.
+ */
+int sparrow_append_kv(const sparrow_shape_t *shape, const void *k_new, const void *v_new,
+                      void *k_cache, void *v_cache, const int32_t *block_table,
+                      const int32_t *seq_lens, void *meta, void *stream);
+
+/*
  * Page scoring and block top-k selection (Sec. 3.3: landmark scores and top-k
  * page picking; Sec. 3.2: the budget from the sparsity schedule).
  *
@@ -161,6 +188,22 @@ int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const v
                             const int32_t *block_table, const int32_t *seq_lens,
                             const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
                             int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * sparrow_append_kv followed by sparrow_page_score_topk, in one pass: the scoring
+ * kernel's workgroup that owns a sequence's last page writes the new K/V rows and that
+ * page's metadata and scores the page from the updated metadata, so no separate
+ * metadata pass runs.  Results (caches, meta, out_k, out_idx) are identical to the two
+ * calls in sequence.  Arguments are those of the two calls; the workspace is that of
+ * SPARROW_OP_SCORE_TOPK.
+ * Errors: as sparrow_page_score_topk, plus SPARROW_EINVAL for a null or misaligned
+ * k_new, v_new, k_cache or v_cache.
+ */
+int sparrow_append_score_topk(const sparrow_shape_t *shape, const void *q, const void *k_new,
+                              const void *v_new, void *k_cache, void *v_cache, void *meta,
+                              const int32_t *block_table, const int32_t *seq_lens,
+                              const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
+                              int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream);
 
 /*
  * Sparse decode attention over the selected pages (block-sparse attention,

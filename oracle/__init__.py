@@ -105,16 +105,23 @@ def page_meta(k_cache, block_table, seq_lens, first_pos=None, meta=None) -> np.n
     return out
 
 
-def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta):
-    """Copies of (k_cache, v_cache, meta) after writing token ``L_b - 1`` of every sequence
-    (rows ``k_new``/``v_new`` ``[B][Hkv][D]``) and rebuilding the metadata of its page."""
+def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta, inplace=False):
+    """(k_cache, v_cache, meta) after writing token ``L_b - 1`` of every sequence (rows
+    ``k_new``/``v_new`` ``[B][Hkv][D]``) and rebuilding the metadata of its page: copies, or
+    the given arrays updated in place (C-contiguous uint16) with ``inplace``."""
     P, Hkv, ps, D = k_cache.shape
     B, max_pages = block_table.shape
     kn, knp = _c(k_new, np.uint16)
     vn, vnp = _c(v_new, np.uint16)
-    kc = np.array(k_cache, dtype=np.uint16, copy=True, order="C")
-    vc = np.array(v_cache, dtype=np.uint16, copy=True, order="C")
-    mt = np.array(meta, dtype=np.uint16, copy=True, order="C")
+    if inplace:
+        for a in (k_cache, v_cache, meta):
+            if a.dtype != np.uint16 or not a.flags.c_contiguous:
+                raise ValueError("in-place append needs C-contiguous uint16 arrays")
+        kc, vc, mt = k_cache, v_cache, meta
+    else:
+        kc = np.array(k_cache, dtype=np.uint16, copy=True, order="C")
+        vc = np.array(v_cache, dtype=np.uint16, copy=True, order="C")
+        mt = np.array(meta, dtype=np.uint16, copy=True, order="C")
     bt, btp = _c(block_table, np.int32)
     sl, slp = _c(seq_lens, np.int32)
     _load().oracle_append_kv(B, Hkv, D, ps, max_pages, knp, vnp, kc.ctypes.data, vc.ctypes.data,

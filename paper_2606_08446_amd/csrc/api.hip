@@ -57,10 +57,30 @@ int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
                                         static_cast<hipStream_t>(stream)));
 }
 
-int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const void *meta,
-                            const int32_t *block_table, const int32_t *seq_lens,
-                            const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
-                            int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream)
+int sparrow_append_kv(const sparrow_shape_t *shape, const void *k_new, const void *v_new,
+                      void *k_cache, void *v_cache, const int32_t *block_table,
+                      const int32_t *seq_lens, void *meta, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!k_new || !v_new || !k_cache || !v_cache || !block_table || !seq_lens || !meta)
+        return SPARROW_EINVAL;
+    if (!al16(k_new) || !al16(v_new) || !al16(k_cache) || !al16(v_cache) || !al16(meta) ||
+        !al4(block_table) || !al4(seq_lens))
+        return SPARROW_EINVAL;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    return status_of(launch_append_kv(*shape, k_new, v_new, k_cache, v_cache, block_table,
+                                      seq_lens, meta, static_cast<hipStream_t>(stream)));
+}
+
+// Shared by sparrow_page_score_topk and sparrow_append_score_topk.
+static int score_topk_call(const sparrow_shape_t *shape, const void *q, void *meta,
+                           const int32_t *block_table, const int32_t *seq_lens,
+                           const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
+                           int32_t *out_idx, void *workspace, size_t ws_bytes,
+                           const AppendArgs &app, void *stream)
 {
     const int rc = check_shape(shape);
     if (rc != SPARROW_OK)
@@ -84,8 +104,37 @@ int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const v
     Sched sched{schedule->bin_tokens, schedule->n_bins, schedule->frac_den, schedule->min_pages,
                 schedule->frac_num};
     return status_of(launch_score_topk(*shape, q, meta, block_table, seq_lens, sched, k_max,
-                                       out_k, out_idx, workspace,
+                                       out_k, out_idx, workspace, app,
                                        static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const void *meta,
+                            const int32_t *block_table, const int32_t *seq_lens,
+                            const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
+                            int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream)
+{
+    const AppendArgs none{nullptr, nullptr, nullptr, nullptr};
+    // Without an append the kernel only reads the metadata.
+    return score_topk_call(shape, q, const_cast<void *>(meta), block_table, seq_lens, schedule,
+                           k_max, out_k, out_idx, workspace, ws_bytes, none, stream);
+}
+
+int sparrow_append_score_topk(const sparrow_shape_t *shape, const void *q, const void *k_new,
+                              const void *v_new, void *k_cache, void *v_cache, void *meta,
+                              const int32_t *block_table, const int32_t *seq_lens,
+                              const sparrow_schedule_t *schedule, int32_t k_max, int32_t *out_k,
+                              int32_t *out_idx, void *workspace, size_t ws_bytes, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!k_new || !v_new || !k_cache || !v_cache)
+        return SPARROW_EINVAL;
+    if (!al16(k_new) || !al16(v_new) || !al16(k_cache) || !al16(v_cache))
+        return SPARROW_EINVAL;
+    const AppendArgs app{k_new, v_new, k_cache, v_cache};
+    return score_topk_call(shape, q, meta, block_table, seq_lens, schedule, k_max, out_k, out_idx,
+                           workspace, ws_bytes, app, stream);
 }
 
 int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, const void *k_cache,

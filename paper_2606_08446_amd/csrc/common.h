@@ -59,6 +59,44 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
 // One fp32 value -> bf16 bits (round to nearest even).
 __device__ __forceinline__ uint32_t to_bf16_bits(float x) { return pack_bf16(x, 0.f) & 0xffffu; }
 
+// bf16 bit pattern -> signed integer with the same order as the values (-0 < +0).
+__device__ __forceinline__ int32_t order16(uint32_t bits)
+{
+    const int32_t s = (int32_t)(int16_t)(uint16_t)bits;
+    return s ^ ((s >> 15) & 0x7fff);
+}
+
+// Inverse of order16 (the map is an involution on 16-bit patterns).
+__device__ __forceinline__ uint32_t unorder16(int32_t key)
+{
+    return (uint32_t)(key ^ ((key >> 15) & 0x7fff)) & 0xffffu;
+}
+
+// Metadata of a page after one more key: 8 bf16 elements of the [mn | mx] row.  `old` is
+// the current slice (min row if !is_max, else max row), `key` the new key's 8 channels;
+// a fresh page (its first token) takes the key itself.  Exact: the result is an input
+// pattern under the total order -0 < +0.
+__device__ __forceinline__ u32x4_t meta_with_key(u32x4_t old, u32x4_t key, bool is_max,
+                                                 bool fresh)
+{
+    if (fresh)
+        return key;
+    u32x4_t r;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        uint32_t out = 0;
+#pragma unroll
+        for (int hw = 0; hw < 2; ++hw) {
+            const int32_t a = order16(old[w] >> (16 * hw));
+            const int32_t k = order16(key[w] >> (16 * hw));
+            const int32_t m = is_max ? max(a, k) : min(a, k);
+            out |= unorder16(m) << (16 * hw);
+        }
+        r[w] = out;
+    }
+    return r;
+}
+
 // Sequence length clamped to what the block table can address.
 __device__ __forceinline__ int clamp_len(int L, int ps, int max_pages)
 {
@@ -95,11 +133,24 @@ hipError_t launch_meta_update(const sparrow_shape_t &s, const void *k_cache,
                               const int32_t *block_table, const int32_t *seq_lens,
                               const int32_t *first_pos, void *meta, hipStream_t stream);
 
+hipError_t launch_append_kv(const sparrow_shape_t &s, const void *k_new, const void *v_new,
+                            void *k_cache, void *v_cache, const int32_t *block_table,
+                            const int32_t *seq_lens, void *meta, hipStream_t stream);
+
+// Token append folded into scoring (k_new == nullptr: no append).
+struct AppendArgs {
+    const void *k_new;
+    const void *v_new;
+    void *k_cache;
+    void *v_cache;
+};
+
 size_t score_topk_workspace(const sparrow_shape_t &s);
-hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void *meta,
+hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta,
                              const int32_t *block_table, const int32_t *seq_lens,
                              const Sched &sched, int32_t k_max, int32_t *out_k,
-                             int32_t *out_idx, void *workspace, hipStream_t stream);
+                             int32_t *out_idx, void *workspace, const AppendArgs &app,
+                             hipStream_t stream);
 
 struct AttnPlan {
     size_t plan_bytes;       // page offsets and unit wave ranges at the start of the workspace

@@ -15,19 +15,6 @@ namespace {
 
 constexpr int kMetaThreads = 128;
 
-// bf16 bit pattern -> signed integer with the same order as the values (-0 < +0).
-__device__ __forceinline__ int32_t order16(uint32_t bits)
-{
-    const int32_t s = (int32_t)(int16_t)(uint16_t)bits;
-    return s ^ ((s >> 15) & 0x7fff);
-}
-
-// Inverse of order16 (the map is an involution on 16-bit patterns).
-__device__ __forceinline__ uint32_t unorder16(int32_t key)
-{
-    return (uint32_t)(key ^ ((key >> 15) & 0x7fff)) & 0xffffu;
-}
-
 __device__ __forceinline__ void fold(u32x4_t v, int32_t (&mn)[8], int32_t (&mx)[8])
 {
 #pragma unroll

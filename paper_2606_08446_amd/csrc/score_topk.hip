@@ -58,6 +58,19 @@ __device__ __forceinline__ float butterfly8(const float (&v)[8], int li)
     return r;
 }
 
+// One lane's share of a page's dot product: its 8 metadata elements against its 8 weights,
+// in a fixed FMA order.
+__device__ __forceinline__ float lane_dot(const float (&w)[8], u32x4_t v)
+{
+    float acc = 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        acc = fmaf(w[2 * t], bf16_lo(v[t]), acc);
+        acc = fmaf(w[2 * t + 1], bf16_hi(v[t]), acc);
+    }
+    return acc;
+}
+
 // One workgroup scores kScorePages consecutive logical pages of one sequence for up to
 // kScoreHeads KV heads.  A wave owns a pair of KV heads: each load instruction reads the
 // two heads' metadata rows of one page, 1 KiB contiguous (lanes 0-31 the first head,
@@ -65,17 +78,25 @@ __device__ __forceinline__ float butterfly8(const float (&v)[8], int li)
 // multiplies its 8 bf16 elements by its 8 fp32 weights (Q- for the mn half, Q+ for the mx
 // half, built from the group's queries) in a fixed FMA chain; butterfly8 then completes
 // the dot products of a batch of 8 pages.  Batches are double-buffered in registers.
+//
+// With kAppend (sparrow_append_score_topk) the token being decoded is appended first: the
+// wave that scores a sequence's last page writes the new key/value rows of its two heads
+// and the page's updated metadata (lane slices of [mn | mx] are exactly the slices
+// meta_with_key works on), and scores that page from the updated slice it holds.
+template <bool kAppend>
 __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ meta,
     const int32_t *__restrict__ block_table, const int32_t *__restrict__ seq_lens, Sched sched,
-    int k_max, int num_q_heads, int num_kv_heads, int ps, int max_pages, float *__restrict__ scores)
+    int k_max, int num_q_heads, int num_kv_heads, int ps, int max_pages,
+    float *__restrict__ scores, AppendArgs app)
 {
     __shared__ int32_t s_phys[kScorePages];
 
     const int b = blockIdx.y;
     const int h0 = blockIdx.z * kScoreHeads;
     const int nh = min(kScoreHeads, num_kv_heads - h0);
-    const int L = clamp_len(seq_lens[b], ps, max_pages);
+    const int L_raw = seq_lens[b];
+    const int L = clamp_len(L_raw, ps, max_pages);
     const int n = (L + ps - 1) / ps;
     const int page0 = blockIdx.x * kScorePages;
     if (page0 >= n)
@@ -120,6 +141,33 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
             }
         }
     }
+    // Append of the token being decoded (position L - 1, on the last page n - 1).
+    int last_slot = -1;  // slot of the appended page in this workgroup, for this lane
+    u32x4_t upd = {0u, 0u, 0u, 0u};
+    if (kAppend && L_raw >= 1 && L_raw <= ps * max_pages) {
+        const int slot = n - 1 - page0;
+        if (slot < npg && active && sub == slot % wpp && head < nh) {
+            const int hh = h0 + head;
+            const int tok = L - 1 - (n - 1) * ps;  // slot of the token within its page
+            const int i0 = e0 & (kHeadDim - 1);
+            const int64_t phys = block_table[(int64_t)b * max_pages + n - 1];
+            const int64_t nrow = ((int64_t)b * num_kv_heads + hh) * kHeadDim + i0;
+            const u32x4_t kn = ld16(static_cast<const uint16_t *>(app.k_new) + nrow);
+            const int64_t crow = ((phys * num_kv_heads + hh) * ps + tok) * kHeadDim + i0;
+            if (e0 < kHeadDim)
+                st16(static_cast<uint16_t *>(app.k_cache) + crow, kn);
+            else
+                st16(static_cast<uint16_t *>(app.v_cache) + crow,
+                     ld16(static_cast<const uint16_t *>(app.v_new) + nrow));
+            // The metadata row of this page is read and written only here.
+            uint16_t *mrow = const_cast<uint16_t *>(meta) +
+                             (phys * num_kv_heads + hh) * 2 * kHeadDim + e0;
+            upd = meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim, tok == 0);
+            st16(mrow, upd);
+            last_slot = slot;
+        }
+    }
+
     // Only now is the budget needed to decide whether this sequence is scored at all.
     if (budget_pages(L, ps, sched, k_max) >= n)
         return;  // every page is kept: nothing to score
@@ -155,19 +203,27 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
             load_batch(j0 + kScoreBatch, nxt);
         float part[kScoreBatch];
 #pragma unroll
-        for (int j = 0; j < kScoreBatch; ++j) {
-            float acc = 0.f;
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                acc = fmaf(w[2 * t], bf16_lo(cur[j][t]), acc);
-                acc = fmaf(w[2 * t + 1], bf16_hi(cur[j][t]), acc);
-            }
-            part[j] = acc;
-        }
+        for (int j = 0; j < kScoreBatch; ++j)
+            part[j] = lane_dot(w, cur[j]);
         const float total = butterfly8(part, li);
         const int j = j0 + (li & 7);
-        if (li < kScoreBatch && j < my_pages && head < nh)
+        // (the appended page was read here before its update landed: its score is
+        // written below instead)
+        if (li < kScoreBatch && j < my_pages && head < nh &&
+            !(kAppend && sub + wpp * j == last_slot))
             out[sub + wpp * j] = total;
+    }
+    if (kAppend && last_slot >= 0) {
+        // Score of the appended page from the updated slice: the same per-lane FMA chain,
+        // and a 32-lane xor reduction (1, 2, 4, 8, 16) - the same tree of additions that
+        // butterfly8 applies to every page, so the score is bit-identical to scoring the
+        // updated metadata from memory.
+        float total = lane_dot(w, upd);
+#pragma unroll
+        for (int x = 1; x < 32; x <<= 1)
+            total += __shfl_xor(total, x, 64);
+        if (li == 0)
+            out[last_slot] = total;
     }
 }
 
@@ -393,19 +449,26 @@ size_t score_topk_workspace(const sparrow_shape_t &s)
     return (size_t)s.batch * s.num_kv_heads * s.max_pages_per_seq * sizeof(float);
 }
 
-hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, const void *meta,
+hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta,
                              const int32_t *block_table, const int32_t *seq_lens,
                              const Sched &sched, int32_t k_max, int32_t *out_k,
-                             int32_t *out_idx, void *workspace, hipStream_t stream)
+                             int32_t *out_idx, void *workspace, const AppendArgs &app,
+                             hipStream_t stream)
 {
     float *scores = static_cast<float *>(workspace);
     const int units = s.batch * s.num_kv_heads;
     const dim3 sgrid((s.max_pages_per_seq + kScorePages - 1) / kScorePages, s.batch,
                      (s.num_kv_heads + kScoreHeads - 1) / kScoreHeads);
-    hipLaunchKernelGGL(k_page_score, sgrid, dim3(kScoreThreads), 0, stream,
-                       static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
-                       block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
-                       s.page_size, s.max_pages_per_seq, scores);
+    if (app.k_new != nullptr)
+        hipLaunchKernelGGL(k_page_score<true>, sgrid, dim3(kScoreThreads), 0, stream,
+                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
+                           block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
+                           s.page_size, s.max_pages_per_seq, scores, app);
+    else
+        hipLaunchKernelGGL(k_page_score<false>, sgrid, dim3(kScoreThreads), 0, stream,
+                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
+                           block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
+                           s.page_size, s.max_pages_per_seq, scores, app);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;

@@ -34,8 +34,9 @@ SPARROW_OP_SCORE_TOPK = 0
 SPARROW_OP_SPARSE_ATTN = 1
 SPARROW_OP_DENSE_ATTN = 2
 
-EXPORTS = ("sparrow_page_meta_update", "sparrow_page_score_topk", "sparrow_sparse_decode_attn",
-           "sparrow_dense_decode_attn", "sparrow_workspace_size", "sparrow_status_string")
+EXPORTS = ("sparrow_page_meta_update", "sparrow_append_kv", "sparrow_page_score_topk",
+           "sparrow_append_score_topk", "sparrow_sparse_decode_attn", "sparrow_dense_decode_attn",
+           "sparrow_workspace_size", "sparrow_status_string")
 
 
 class SparrowError(RuntimeError):
@@ -79,7 +80,11 @@ def load():
                                                ctypes.c_float, _p, _i32, _p, ctypes.c_size_t, _p]
     lib.sparrow_dense_decode_attn.argtypes = [sp, _p, _p, _p, _p, _p, ctypes.c_float, _p, _i32,
                                               _p, ctypes.c_size_t, _p]
-    for fn in EXPORTS[:4]:
+    lib.sparrow_append_kv.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _p]
+    lib.sparrow_append_score_topk.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _p,
+                                              ctypes.POINTER(Schedule), _i32, _p, _p, _p,
+                                              ctypes.c_size_t, _p]
+    for fn in EXPORTS[:6]:
         getattr(lib, fn).restype = ctypes.c_int
     lib.sparrow_workspace_size.argtypes = [sp, _i32, _i32]
     lib.sparrow_workspace_size.restype = ctypes.c_size_t
@@ -100,6 +105,20 @@ def sparrow_page_score_topk(shape, q, meta, block_table, seq_lens, schedule, k_m
     return load().sparrow_page_score_topk(ctypes.byref(shape), q, meta, block_table, seq_lens,
                                           ctypes.byref(schedule), k_max, out_k, out_idx,
                                           workspace, ws_bytes, stream)
+
+
+def sparrow_append_kv(shape, k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta, stream):
+    return load().sparrow_append_kv(ctypes.byref(shape), k_new, v_new, k_cache, v_cache,
+                                    block_table, seq_lens, meta, stream)
+
+
+def sparrow_append_score_topk(shape, q, k_new, v_new, k_cache, v_cache, meta, block_table,
+                              seq_lens, schedule, k_max, out_k, out_idx, workspace, ws_bytes,
+                              stream):
+    return load().sparrow_append_score_topk(ctypes.byref(shape), q, k_new, v_new, k_cache,
+                                            v_cache, meta, block_table, seq_lens,
+                                            ctypes.byref(schedule), k_max, out_k, out_idx,
+                                            workspace, ws_bytes, stream)
 
 
 def sparrow_sparse_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens, k, idx, k_max,
@@ -192,6 +211,17 @@ def page_meta_update(k_cache, block_table, seq_lens, meta, first_pos=None, shape
                                   _ptr(first_pos), _ptr(meta), _stream(k_cache.device))
     _check("sparrow_page_meta_update", rc)
     return meta
+
+
+def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta):
+    """Write token ``seq_lens[b] - 1`` of every sequence into the caches and update the
+    metadata of its page (all in place)."""
+    _require_device(k_cache)
+    P, Hkv, ps, D = k_cache.shape
+    shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D)
+    rc = sparrow_append_kv(shape, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+                           _ptr(block_table), _ptr(seq_lens), _ptr(meta), _stream(k_cache.device))
+    _check("sparrow_append_kv", rc)
 
 
 def page_score_topk(q, meta, block_table, seq_lens, k_cache_shape, min_pages, frac_num,
@@ -291,21 +321,40 @@ class SparseDecodeStep:
         self.ws_attn = _workspace(sparrow_workspace_size(self.shape, self.k_max,
                                                          SPARROW_OP_SPARSE_ATTN), dev)
 
-    def meta_update(self, first_pos, stream):
+    # Every method takes an optional ``seq_lens`` tensor that replaces the one given at
+    # construction for that call (a decode loop advances the lengths step by step).
+    def _lens(self, seq_lens):
+        return _ptr(self.seq_lens if seq_lens is None else seq_lens)
+
+    def meta_update(self, first_pos, stream, seq_lens=None):
         _check("sparrow_page_meta_update", sparrow_page_meta_update(
-            self.shape, _ptr(self.k_cache), _ptr(self.block_table), _ptr(self.seq_lens),
+            self.shape, _ptr(self.k_cache), _ptr(self.block_table), self._lens(seq_lens),
             _ptr(first_pos), _ptr(self.meta), stream))
 
-    def score_topk(self, stream):
+    def append(self, k_new, v_new, stream, seq_lens=None):
+        """Write the decoded token's K/V rows and update its page's metadata."""
+        _check("sparrow_append_kv", sparrow_append_kv(
+            self.shape, _ptr(k_new), _ptr(v_new), _ptr(self.k_cache), _ptr(self.v_cache),
+            _ptr(self.block_table), self._lens(seq_lens), _ptr(self.meta), stream))
+
+    def score_topk(self, stream, seq_lens=None):
         _check("sparrow_page_score_topk", sparrow_page_score_topk(
             self.shape, _ptr(self.q), _ptr(self.meta), _ptr(self.block_table),
-            _ptr(self.seq_lens), self.sched, self.k_max, _ptr(self.k), _ptr(self.idx),
+            self._lens(seq_lens), self.sched, self.k_max, _ptr(self.k), _ptr(self.idx),
             _ptr(self.ws_score), self.ws_score.numel(), stream))
 
-    def attend(self, stream):
+    def append_score_topk(self, k_new, v_new, stream, seq_lens=None):
+        """Append the decoded token (k_new/v_new [B][Hkv][D]) and select pages, fused."""
+        _check("sparrow_append_score_topk", sparrow_append_score_topk(
+            self.shape, _ptr(self.q), _ptr(k_new), _ptr(v_new), _ptr(self.k_cache),
+            _ptr(self.v_cache), _ptr(self.meta), _ptr(self.block_table), self._lens(seq_lens),
+            self.sched, self.k_max, _ptr(self.k), _ptr(self.idx), _ptr(self.ws_score),
+            self.ws_score.numel(), stream))
+
+    def attend(self, stream, seq_lens=None):
         _check("sparrow_sparse_decode_attn", sparrow_sparse_decode_attn(
             self.shape, _ptr(self.q), _ptr(self.k_cache), _ptr(self.v_cache),
-            _ptr(self.block_table), _ptr(self.seq_lens), _ptr(self.k), _ptr(self.idx),
+            _ptr(self.block_table), self._lens(seq_lens), _ptr(self.k), _ptr(self.idx),
             self.k_max, self.scale, _ptr(self.out), SPARROW_OUT_F32, _ptr(self.ws_attn),
             self.ws_attn.numel(), stream))
 

@@ -78,12 +78,24 @@ def call(fn, shape, **over):
         a.update(over)
         return S.sparrow_page_meta_update(shape, a["k_cache"], a["bt"], a["lens"], a["first_pos"],
                                           a["meta"], None)
+    if fn == "append":
+        a = dict(k_new=FAKE, v_new=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, meta=FAKE)
+        a.update(over)
+        return S.sparrow_append_kv(shape, a["k_new"], a["v_new"], a["k"], a["v"], a["bt"],
+                                   a["lens"], a["meta"], None)
     if fn == "topk":
         a = dict(q=FAKE, meta=FAKE, bt=FAKE, lens=FAKE, sched=sched(), k_max=8, out_k=FAKE,
                  out_idx=FAKE)
         a.update(over)
         return S.sparrow_page_score_topk(shape, a["q"], a["meta"], a["bt"], a["lens"], a["sched"],
                                          a["k_max"], a["out_k"], a["out_idx"], ws, ws_bytes, None)
+    if fn == "fused":
+        a = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k=FAKE, v=FAKE, meta=FAKE, bt=FAKE, lens=FAKE,
+                 sched=sched(), k_max=8, out_k=FAKE, out_idx=FAKE)
+        a.update(over)
+        return S.sparrow_append_score_topk(shape, a["q"], a["k_new"], a["v_new"], a["k"], a["v"],
+                                           a["meta"], a["bt"], a["lens"], a["sched"], a["k_max"],
+                                           a["out_k"], a["out_idx"], ws, ws_bytes, None)
     if fn == "sparse":
         a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, kk=FAKE, idx=FAKE, k_max=8,
                  out=FAKE, dtype=0)
@@ -97,7 +109,7 @@ def call(fn, shape, **over):
                                        a["out"], a["dtype"], ws, ws_bytes, None)
 
 
-@pytest.mark.parametrize("fn", ["meta", "topk", "sparse", "dense"])
+@pytest.mark.parametrize("fn", ["meta", "append", "topk", "fused", "sparse", "dense"])
 @pytest.mark.parametrize("bad,status", BAD_SHAPES)
 def test_bad_shapes_are_rejected(lib, fn, bad, status):
     bad = dict(bad)
@@ -109,7 +121,9 @@ def test_bad_shapes_are_rejected(lib, fn, bad, status):
 
 NULLS = {
     "meta": ["k_cache", "bt", "lens", "meta"],
+    "append": ["k_new", "v_new", "k", "v", "bt", "lens", "meta"],
     "topk": ["q", "meta", "bt", "lens", "out_k", "out_idx"],
+    "fused": ["q", "k_new", "v_new", "k", "v", "meta", "bt", "lens", "out_k", "out_idx"],
     "sparse": ["q", "k", "v", "bt", "lens", "kk", "idx", "out"],
     "dense": ["q", "k", "v", "bt", "lens", "out"],
 }
@@ -127,6 +141,9 @@ def test_null_shape_and_schedule_are_rejected(lib):
     assert call("topk", good_shape(), sched=S.Schedule(2048, 1, FAKE, FAKE, 0)) == S.SPARROW_EINVAL
     assert call("topk", good_shape(), sched=S.Schedule(2048, 1, None, FAKE, 10)) == S.SPARROW_EINVAL
     assert call("topk", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    assert call("fused", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    assert call("fused", good_shape(), sched=S.Schedule(2048, 1, FAKE, None, 10)) == \
+        S.SPARROW_EINVAL
     assert call("sparse", good_shape(), k_max=0) == S.SPARROW_EINVAL
 
 
@@ -136,6 +153,7 @@ def test_unsupported_output_dtype(lib):
 
 
 @pytest.mark.parametrize("fn,op", [("topk", S.SPARROW_OP_SCORE_TOPK),
+                                   ("fused", S.SPARROW_OP_SCORE_TOPK),
                                    ("sparse", S.SPARROW_OP_SPARSE_ATTN),
                                    ("dense", S.SPARROW_OP_DENSE_ATTN)])
 def test_workspace_checks(lib, fn, op):
@@ -148,7 +166,7 @@ def test_workspace_checks(lib, fn, op):
 
 def test_empty_batch_enqueues_nothing(lib):
     shape = good_shape(batch=0)
-    for fn in ("meta", "topk", "sparse", "dense"):
+    for fn in ("meta", "append", "topk", "fused", "sparse", "dense"):
         assert call(fn, shape, ws=None, ws_bytes=0) == S.SPARROW_OK
 
 
@@ -190,7 +208,8 @@ def test_tensor_wrappers_refuse_host_tensors():
                             torch.zeros(1, 2, dtype=torch.int32), torch.ones(1, dtype=torch.int32))
 
 
-VEC16 = {"meta": ["k_cache", "meta"], "topk": ["q", "meta", "ws"],
+VEC16 = {"meta": ["k_cache", "meta"], "append": ["k_new", "v_new", "k", "v", "meta"],
+         "topk": ["q", "meta", "ws"], "fused": ["q", "k_new", "v_new", "k", "v", "meta", "ws"],
          "sparse": ["q", "k", "v", "out", "ws"], "dense": ["q", "k", "v", "out", "ws"]}
 
 

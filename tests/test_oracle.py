@@ -146,6 +146,12 @@ def test_append_writes_exactly_one_row_per_head_and_rebuilds_its_page():
                                           rows[np.argmin(keys, 0), np.arange(D)])
             np.testing.assert_array_equal(mt[phys, h, 1],
                                           rows[np.argmax(keys, 0), np.arange(D)])
+    # the in-place form gives the same arrays
+    kc2, vc2, mt2 = d["k"].copy(), d["v"].copy(), meta0.copy()
+    oracle.append_kv(kn, vn, kc2, vc2, d["bt"], lens, mt2, inplace=True)
+    np.testing.assert_array_equal(kc2, kc)
+    np.testing.assert_array_equal(vc2, vc)
+    np.testing.assert_array_equal(mt2, mt)
     # pages nobody appended to keep their metadata
     untouched = np.ones(mt.shape[0], bool)
     untouched[[t[1] for t in touched]] = False
