@@ -45,6 +45,11 @@ def parse():
     ap.add_argument("--step", choices=("fused", "separate"), default="fused",
                     help="fused: sparrow_append_score_topk + attention; separate: "
                          "sparrow_append_kv, sparrow_page_score_topk, attention")
+    ap.add_argument("--layers", type=int, default=1,
+                    help="attention layers per step, each with its own cache (value stays per "
+                         "layer: batch x layers / step time)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the whole step captured in one HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for counter scaling)")
     return ap.parse_args()
@@ -215,50 +220,79 @@ def main():
     ps = w.page_size
     # every step appends one token per sequence: spare pages for all of them
     w = dataclasses.replace(w, extra_pages=(Wm + K + 1 + ps - 1) // ps + 1)
-    inp = W.generate(w, dev)
+    L_layers = args.layers
     s = w.schedule
     B, Hkv = w.batch, w.num_kv_heads
     total = Wm + K
-    # step i appends the token at position lens0 + i: its lengths are lens0 + i + 1
-    lens0 = inp.seq_lens.clone()
-    lens_steps = (lens0[None, :] + torch.arange(1, total + 1, device=dev,
-                                                dtype=torch.int32)[:, None]).contiguous()
-    lens_host_steps = inp.lens_host[None, :] + np.arange(1, total + 1)[:, None]
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(w.seed + 1)
-    k_new = torch.randn((total, B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
-    v_new = torch.randn((total, B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
-    k_max = S.budget_bound(lens_host_steps.ravel(), ps, s.bin_tokens, s.min_pages, s.frac_num,
-                           s.frac_den)
-    meta = torch.zeros((inp.num_phys_pages, Hkv, 2, 128), dtype=torch.bfloat16, device=dev)
-    S.page_meta_update(inp.k_cache, inp.block_table, lens0, meta)
-    step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table, lens0,
-                              meta, inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, k_max)
-    dense_out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
-    dense_ws = torch.empty(max(16, S.sparrow_workspace_size(step.shape, 0,
-                                                            S.SPARROW_OP_DENSE_ATTN)),
-                           dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream(dev)
-    sp = stream.cuda_stream
     fused = args.step == "fused"
 
-    def select(i):
-        if fused:
-            step.append_score_topk(k_new[i], v_new[i], sp, seq_lens=lens_steps[i])
-        else:
-            step.append(k_new[i], v_new[i], sp, seq_lens=lens_steps[i])
-            step.score_topk(sp, seq_lens=lens_steps[i])
+    class Layer:
+        """One attention layer: its own cache, metadata and new rows; the lengths (and so
+        the schedule) are shared by all layers, as in a model."""
+
+        def __init__(self, li, lengths):
+            seed = w.seed + 1000 * li
+            # layer 0 is the workload itself; the others reuse its lengths
+            self.inp = W.generate(w, dev, lengths=None if li == 0 else lengths, seed=seed)
+            assert list(self.inp.lens_host) == list(lengths)
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(seed + 1)
+            self.k_new = torch.randn((total, B, Hkv, 128), generator=gen,
+                                     device=dev).to(torch.bfloat16)
+            self.v_new = torch.randn((total, B, Hkv, 128), generator=gen,
+                                     device=dev).to(torch.bfloat16)
+            inp = self.inp
+            self.meta = torch.zeros((inp.num_phys_pages, Hkv, 2, 128), dtype=torch.bfloat16,
+                                    device=dev)
+            S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, self.meta)
+            self.step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table,
+                                           inp.seq_lens, self.meta, inp.min_pages, inp.frac_num,
+                                           s.frac_den, s.bin_tokens, k_max)
+            self.dense_out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
+            self.dense_ws = torch.empty(max(16, S.sparrow_workspace_size(
+                self.step.shape, 0, S.SPARROW_OP_DENSE_ATTN)), dtype=torch.uint8, device=dev)
+
+        def select(self, i, sp):
+            st = self.step
+            if fused:
+                st.append_score_topk(self.k_new[i], self.v_new[i], sp, seq_lens=lens_steps[i])
+            else:
+                st.append(self.k_new[i], self.v_new[i], sp, seq_lens=lens_steps[i])
+                st.score_topk(sp, seq_lens=lens_steps[i])
+
+        def sparse(self, i, sp):
+            self.select(i, sp)
+            self.step.attend(sp, seq_lens=lens_steps[i])
+
+        def dense(self, i, sp):
+            st, inp = self.step, self.inp
+            st.append(self.k_new[i], self.v_new[i], sp, seq_lens=lens_steps[i])
+            S._check("sparrow_dense_decode_attn", S.sparrow_dense_decode_attn(
+                st.shape, inp.q.data_ptr(), inp.k_cache.data_ptr(), inp.v_cache.data_ptr(),
+                inp.block_table.data_ptr(), lens_steps[i].data_ptr(), st.scale,
+                self.dense_out.data_ptr(), S.SPARROW_OUT_F32, self.dense_ws.data_ptr(),
+                self.dense_ws.numel(), sp))
+
+    # the lengths the workload generator draws first from its seed
+    lens_host0 = np.random.default_rng(w.seed).integers(w.len_lo, w.len_hi + 1,
+                                                        size=B).astype(np.int64)
+    # step i appends the token at position lens0 + i: its lengths are lens0 + i + 1
+    lens_host_steps = lens_host0[None, :] + np.arange(1, total + 1)[:, None]
+    lens_steps = torch.as_tensor(lens_host_steps.astype(np.int32), device=dev).contiguous()
+    k_max = S.budget_bound(lens_host_steps.ravel(), ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den)
+    layers = [Layer(li, list(lens_host0)) for li in range(L_layers)]
+    inp, step = layers[0].inp, layers[0].step
+    stream = torch.cuda.current_stream(dev)
+    sp = stream.cuda_stream
 
     def sparse_step(i):
-        select(i)
-        step.attend(sp, seq_lens=lens_steps[i])
+        for lay in layers:
+            lay.sparse(i, sp)
 
     def dense_step(i):
-        step.append(k_new[i], v_new[i], sp, seq_lens=lens_steps[i])
-        S._check("sparrow_dense_decode_attn", S.sparrow_dense_decode_attn(
-            step.shape, inp.q.data_ptr(), inp.k_cache.data_ptr(), inp.v_cache.data_ptr(),
-            inp.block_table.data_ptr(), lens_steps[i].data_ptr(), step.scale,
-            dense_out.data_ptr(), S.SPARROW_OUT_F32, dense_ws.data_ptr(), dense_ws.numel(), sp))
+        for lay in layers:
+            lay.dense(i, sp)
 
     def timed(fn, first, count):
         e0 = torch.cuda.Event(enable_timing=True)
@@ -271,31 +305,54 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / count
 
+    def captured(fn, i):
+        """fn(i) for every layer captured in one graph; returns a replay callable."""
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                csp = torch.cuda.current_stream().cuda_stream
+                for lay in layers:
+                    fn(lay, i, csp)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        return lambda _i: g.replay()
+
     for i in range(Wm):
         sparse_step(i)
     torch.cuda.synchronize()
 
     # ---- timed sparse steps: exactly K steps between two events, nothing else inside
+    if args.graph:
+        # the graph holds the step at index Wm (all layers); each replay re-appends the same
+        # token, which leaves caches and metadata unchanged: the same work every replay
+        sparse_fn = captured(Layer.sparse, Wm)
+        dense_fn = captured(Layer.dense, Wm)
+    else:
+        sparse_fn, dense_fn = sparse_step, dense_step
     t_wall = time.perf_counter()
-    ms_step = timed(sparse_step, Wm, K)
+    ms_step = timed(sparse_fn, Wm, K)
     wall = time.perf_counter() - t_wall
     k_host = step.k.cpu().numpy()
     idx_host = step.idx.cpu().numpy()
 
-    # ---- per-entry-point durations (a separate loop over the same steps; re-running a step
-    # rewrites the same token, which leaves caches and metadata unchanged)
+    # ---- per-entry-point durations of layer 0 (a separate loop over the same steps;
+    # re-running a step rewrites the same token, which leaves caches and metadata unchanged)
+    lay0 = layers[0]
     phase = {}
     if fused:
-        phase["append_score_topk"] = timed(select, Wm, K)
+        phase["append_score_topk"] = timed(lambda i: lay0.select(i, sp), Wm, K)
     else:
-        phase["append"] = timed(lambda i: step.append(k_new[i], v_new[i], sp,
+        phase["append"] = timed(lambda i: step.append(lay0.k_new[i], lay0.v_new[i], sp,
                                                       seq_lens=lens_steps[i]), Wm, K)
         phase["score_topk"] = timed(lambda i: step.score_topk(sp, seq_lens=lens_steps[i]), Wm, K)
     phase["sparse_attn"] = timed(lambda i: step.attend(sp, seq_lens=lens_steps[i]), Wm, K)
 
     # ---- timed dense steps over the same appended tokens
-    ms_dense = timed(dense_step, Wm, K)
-
+    ms_dense = timed(dense_fn, Wm, K)
+    if args.graph:
+        lens_host_steps = lens_host_steps[:Wm + 1]  # every replay ran step Wm
     lens_last = lens_host_steps[-1]
     by = sparse_bytes(inp, lens_last, k_host, idx_host)
     if fused:
@@ -303,15 +360,16 @@ def main():
               "sparse_attn": by["sparse_attn"]}
     total_bytes = sum(by.values())
     dbytes = dense_bytes(inp, lens_last)
-    gbps = total_bytes / (ms_step * 1e-3) / 1e9
-    dgbps = dbytes / (ms_dense * 1e-3) / 1e9
+    gbps = total_bytes * L_layers / (ms_step * 1e-3) / 1e9
+    dgbps = dbytes * L_layers / (ms_dense * 1e-3) / 1e9
     dominant = max(phase, key=phase.get)
     dom_gbps = by[dominant] / (phase[dominant] * 1e-3) / 1e9
     traffic = read_traffic(source_sha(), w.name) if dominant == "sparse_attn" else None
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(inp, lens_last, k_new[-1], v_new[-1], k_max, args.cpu_seconds)
+        cpu = cpu_baseline(inp, lens_last, lay0.k_new[len(lens_host_steps) - 1],
+                           lay0.v_new[len(lens_host_steps) - 1], k_max, args.cpu_seconds)
 
     budgets = np.asarray(k_host)
     kernels = {"sparse_attn": "k_attn_stream<sparse> + k_attn_merge",
@@ -319,7 +377,7 @@ def main():
                "score_topk": "k_page_score + k_topk", "append": "k_append_kv"}
     result = {
         "metric": METRIC,
-        "value": round(B / (ms_step * 1e-3), 2),
+        "value": round(B * L_layers / (ms_step * 1e-3), 2),
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": K,
@@ -334,7 +392,8 @@ def main():
                    "num_kv_heads": Hkv, "head_dim": 128, "page_size": ps,
                    "len_range": [w.len_lo, w.len_hi], "budget_pages": [int(budgets.min()),
                                                                        int(budgets.max())],
-                   "k_max": int(k_max),
+                   "k_max": int(k_max), "layers": L_layers,
+                   "graph": bool(args.graph),
                    "step": ("append+score+top-k fused, attention" if fused else
                             "append, score+top-k, attention") +
                            "; one token appended per sequence per step"},
@@ -342,7 +401,8 @@ def main():
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": {k: int(v) for k, v in by.items()},
         "phase_ms": {k: round(v, 5) for k, v in phase.items()},
-        "dense": {"queries_per_s": round(B / (ms_dense * 1e-3), 2), "ms_per_step": round(ms_dense, 5),
+        "dense": {"queries_per_s": round(B * L_layers / (ms_dense * 1e-3), 2),
+                  "ms_per_step": round(ms_dense, 5),
                   "bytes_per_step": int(dbytes), "achieved_GBps": round(dgbps, 1),
                   "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4),
                   "step": "append, dense attention"},
