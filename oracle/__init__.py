@@ -52,6 +52,13 @@ def _load():
     lib.oracle_attention.restype = None
     lib.oracle_weight_sum.argtypes = [_i32, ctypes.c_int64, _p, _p, ctypes.c_double]
     lib.oracle_weight_sum.restype = ctypes.c_double
+    lib.oracle_acceptance.argtypes = [ctypes.c_int64, _i32, _i32, _p, _p, ctypes.c_double, _p]
+    lib.oracle_acceptance.restype = None
+    lib.oracle_acceptance_topk.argtypes = [ctypes.c_int64, _i32, _p, _p, _p]
+    lib.oracle_acceptance_topk.restype = None
+    lib.oracle_tail_stats.argtypes = [ctypes.c_int64, _p, _p, _i32, _i32, ctypes.c_double, _p, _p,
+                                      _p]
+    lib.oracle_tail_stats.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = _i32
     _lib = lib
@@ -209,3 +216,43 @@ def sparse_step(q, k_cache, v_cache, block_table, seq_lens, schedule, k_max, sca
     idx = select(seq_lens, k, s32, ps, k_max)
     out = attention(q, k_cache, v_cache, block_table, seq_lens, scale, k, idx)
     return {"meta": meta, "scores32": s32, "scores64": s64, "k": k, "idx": idx, "out": out}
+
+
+# ----------------------------------------------------------------- acceptance rate (Sec. 3.1)
+def acceptance(target, draft, inv_temp=1.0) -> np.ndarray:
+    """Per-token acceptance rate ``sum_x min(p(x), q(x))`` (Eq. 1), fp64 ``[T]``.
+
+    ``target``/``draft``: logit rows ``[T][V]``, float32 or bf16 bit patterns (uint16)."""
+    if target.dtype == np.uint16:
+        dtype, npt = 1, np.uint16
+    else:
+        dtype, npt = 0, np.float32
+    tg, tgp = _c(target, npt)
+    dr, drp = _c(draft, npt)
+    T, V = tg.shape
+    out = np.zeros(T, np.float64)
+    _load().oracle_acceptance(T, V, dtype, tgp, drp, float(inv_temp), out.ctypes.data)
+    return out
+
+
+def acceptance_topk(lp_target, lp_draft) -> np.ndarray:
+    """The top-K approximation from normalised log-probabilities ``[T][K]`` (fp32)."""
+    a, ap = _c(lp_target, np.float32)
+    b, bp = _c(lp_draft, np.float32)
+    T, K = a.shape
+    out = np.zeros(T, np.float64)
+    _load().oracle_acceptance_topk(T, K, ap, bp, out.ctypes.data)
+    return out
+
+
+def tail_stats(alpha, positions, bin_tokens, n_bins, pct):
+    """(quantile fp64 [n_bins], mean fp64 [n_bins], count int64 [n_bins]) of ``alpha`` (fp32)
+    grouped by position bin; the ``pct``-percentile with linear interpolation."""
+    a, ap = _c(alpha, np.float32)
+    ps_, pp = _c(positions, np.int32)
+    q = np.zeros(n_bins, np.float64)
+    m = np.zeros(n_bins, np.float64)
+    c = np.zeros(n_bins, np.int64)
+    _load().oracle_tail_stats(len(a), ap, pp, int(bin_tokens), int(n_bins), float(pct),
+                              q.ctypes.data, m.ctypes.data, c.ctypes.data)
+    return q, m, c

@@ -283,3 +283,78 @@ def with_schedule(inp: Inputs, w: Workload) -> Inputs:
         inp, workload=w,
         min_pages=torch.as_tensor(np.array(w.schedule.min_pages, np.int32), device=dev),
         frac_num=torch.as_tensor(np.array(w.schedule.frac_num, np.int32), device=dev))
+
+
+# ----------------------------------------------------------------------------------------------
+# Paired logit rows for the per-token acceptance rate (Sec. 3.1): for each generated token, the
+# target (dense policy) and draft (sparse rollout) logits over the vocabulary, and its position.
+# Random inputs only; the acceptance rate itself is computed elsewhere.
+# ----------------------------------------------------------------------------------------------
+@dataclasses.dataclass(frozen=True)
+class LogitWorkload:
+    """Synthetic logit rows: target = scale * N(0, 1) with one chosen token raised by a peak
+    drawn from U(peak_lo, peak_hi) (confident next-token predictions); draft = target +
+    sigma_t * N(0, 1), where sigma_t = noise * exp(noise_sigma * N(0, 1)) * (1 + growth * pos /
+    max_pos) is log-normal per token (most tokens barely perturbed, a heavy tail) and grows with
+    the position, which is uniform in [0, max_pos)."""
+    name: str
+    tokens: int
+    vocab: int
+    max_pos: int
+    bin_tokens: int
+    n_bins: int
+    scale: float = 2.0
+    peak_lo: float = 10.0
+    peak_hi: float = 20.0
+    noise: float = 0.01
+    noise_sigma: float = 2.0
+    growth: float = 2.0
+    dtype: str = "f32"     # "f32" or "bf16"
+    seed: int = 31
+
+
+# Qwen3's vocabulary, 4096 generated tokens over a 40K-token generation in 2K-token bins.
+A1 = LogitWorkload("a1_qwen3_vocab_t4096", 4096, 151936, 40960, 2048, 20)
+A1_BF16 = dataclasses.replace(A1, name="a1_qwen3_vocab_t4096_bf16", dtype="bf16")
+LOGIT_CONFIGS = {"a1": A1, "a1-bf16": A1_BF16}
+
+
+@dataclasses.dataclass
+class LogitInputs:
+    workload: LogitWorkload
+    target: torch.Tensor      # [T][V] float32 or bf16
+    draft: torch.Tensor       # [T][V]
+    positions: torch.Tensor   # int32 [T]
+    sigma: np.ndarray         # float64 [T] perturbation scale of each token
+
+
+def generate_logits(lw: LogitWorkload, device="cpu", chunk_rows: int = 256) -> LogitInputs:
+    rng = np.random.default_rng(lw.seed)
+    T, V = lw.tokens, lw.vocab
+    pos = rng.integers(0, lw.max_pos, size=T).astype(np.int32)
+    peak_id = rng.integers(0, V, size=T)
+    peak = rng.uniform(lw.peak_lo, lw.peak_hi, size=T)
+    sigma = lw.noise * np.exp(lw.noise_sigma * rng.standard_normal(T)) * \
+        (1.0 + lw.growth * pos / lw.max_pos)
+    dt = torch.float32 if lw.dtype == "f32" else torch.bfloat16
+    target = torch.empty((T, V), dtype=dt, device=device)
+    draft = torch.empty((T, V), dtype=dt, device=device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(lw.seed)
+    for r0 in range(0, T, chunk_rows):
+        r1 = min(T, r0 + chunk_rows)
+        z = torch.randn((r1 - r0, V), generator=gen, device=device) * lw.scale
+        rows = torch.arange(r1 - r0, device=device)
+        z[rows, torch.as_tensor(peak_id[r0:r1], device=device)] += \
+            torch.as_tensor(peak[r0:r1], dtype=torch.float32, device=device)
+        e = torch.randn((r1 - r0, V), generator=gen, device=device)
+        s = torch.as_tensor(sigma[r0:r1], dtype=torch.float32, device=device)[:, None]
+        target[r0:r1] = z.to(dt)
+        draft[r0:r1] = (z + s * e).to(dt)
+    return LogitInputs(lw, target, draft, torch.as_tensor(pos, device=device), sigma)
+
+
+def small_logits(T=40, V=3000, seed=0, dtype="f32", **kw) -> LogitWorkload:
+    return LogitWorkload(f"small_logits_t{T}_v{V}", T, V, kw.pop("max_pos", 12000),
+                         kw.pop("bin_tokens", 2048), kw.pop("n_bins", 6), dtype=dtype, seed=seed,
+                         **kw)

@@ -12,7 +12,8 @@ import sys
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SRC = os.path.join(ROOT, "oracle", "sparrow_oracle.c")
+ORACLE = os.path.join(ROOT, "oracle")
+SOURCES = ("sparrow_oracle.c", "acceptance_oracle.c")
 
 MUTANTS = {
     "topk_ties_to_higher_index": ("return (a->p > b->p) - (a->p < b->p);",
@@ -46,18 +47,39 @@ MUTANTS = {
 }
 
 
-@pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_pins_catch_planted_mistake(name, tmp_path):
-    old, new = MUTANTS[name]
-    src = open(SRC).read()
-    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
-    mutant = tmp_path / "sparrow_oracle.c"
-    mutant.write_text(src.replace(old, new))
+# Mistakes in the acceptance-rate oracle: (file, old, new), pinned by test_oracle_acceptance.py.
+ACCEPTANCE_MUTANTS = {
+    "acceptance_max_instead_of_min": (
+        "- Q);\n            a += p < q ? p : q;", "- Q);\n            a += p > q ? p : q;"),
+    "acceptance_lse_without_log_sum": ("    return m + log(s);", "    return m;"),
+    "acceptance_ignores_temperature": (
+        "    for (int32_t x = 0; x < V; ++x)\n        s += exp(tau * logit_value(row, dtype, x) - m);",
+        "    for (int32_t x = 0; x < V; ++x)\n        s += exp(logit_value(row, dtype, x) - m);"),
+    "percentile_nearest_rank": ("quantile[b] = x_lo + (h - (double)lo) * (x_hi - x_lo);",
+                                "quantile[b] = x_lo;"),
+    "tail_bin_not_clamped": ("            if (bin > n_bins - 1)\n                bin = n_bins - 1;",
+                             "            if (bin > n_bins)\n                bin = n_bins - 1;"),
+}
+CASES = [(n, "sparrow_oracle.c", o, w, "test_oracle.py") for n, (o, w) in MUTANTS.items()] + \
+        [(n, "acceptance_oracle.c", o, w, "test_oracle_acceptance.py")
+         for n, (o, w) in ACCEPTANCE_MUTANTS.items()]
+
+
+@pytest.mark.parametrize("name,fname,old,new,pins", sorted(CASES), ids=[c[0] for c in sorted(CASES)])
+def test_pins_catch_planted_mistake(name, fname, old, new, pins, tmp_path):
+    srcs = []
+    for f in SOURCES:
+        text = open(os.path.join(ORACLE, f)).read()
+        if f == fname:
+            assert text.count(old) == 1, f"mutation site for {name} not found exactly once"
+            text = text.replace(old, new)
+        (tmp_path / f).write_text(text)
+        srcs.append(str(tmp_path / f))
     lib = tmp_path / "liboracle_mutant.so"
     subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-fopenmp", "-ffp-contract=off",
-                           "-shared", "-o", str(lib), str(mutant), "-lm"])
+                           "-shared", "-o", str(lib)] + srcs + ["-lm"])
     env = dict(os.environ, SPARROW_ORACLE_LIB=str(lib), OMP_NUM_THREADS="2")
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle.py")],
+                        os.path.join(ROOT, "tests", pins)],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
