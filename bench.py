@@ -38,7 +38,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="c2", help="c1..c5, or c4-2/c4-5/c4-10/c4-25/c4-100")
+    ap.add_argument("--workload", default="c2",
+                    help="c1..c5, or c4-2/c4-5/c4-10/c4-25/c4-100; a1 / a1-bf16 for the "
+                         "acceptance rate over paired logit rows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample")
@@ -116,10 +118,27 @@ def read_traffic(kernel_src_sha, workload_name):
     return float(vals["traffic_bytes_per_launch"])
 
 
-def source_sha():
+def acceptance_traffic(workload_name):
+    """HBM traffic per k_acceptance launch from its committed counter summary, if it matches
+    the current source."""
+    path = os.path.join(ROOT, "profiles", "traffic_acceptance_a1_qwen3_vocab_t4096.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_sha(("acceptance.hip", "common.h")):
+        return None
+    v = vals.get(f"traffic_bytes_per_launch[{workload_name}]")
+    return None if v is None else float(v)
+
+
+def source_sha(files=("attention.hip", "common.h")):
     import hashlib
     h = hashlib.sha256()
-    for f in ("attention.hip", "common.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2606_08446_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -195,6 +214,92 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_each_way": n, "launches": 5}), flush=True)
 
 
+def bench_acceptance(args):
+    """Acceptance rate of every token of a logit workload, then the per-bin tail statistic."""
+    import numpy as np
+    import torch
+
+    from paper_2606_08446_amd import sparrow as S
+    from paper_2606_08446_amd import workloads as W
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    lw = W.LOGIT_CONFIGS[args.workload]
+    li = W.generate_logits(lw, dev)
+    T, V = lw.tokens, lw.vocab
+    esz = 4 if lw.dtype == "f32" else 2
+    alpha = torch.empty(T, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        S.acceptance_rate(li.target, li.draft, 1.0, alpha=alpha)
+        return S.tail_stats(alpha, li.positions, lw.bin_tokens, lw.n_bins, 5.0)
+
+    def timed(fn, count):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(count):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / count
+
+    for _ in range(args.warmup):
+        step()
+    t_wall = time.perf_counter()
+    ms_step = timed(step, args.steps)
+    wall = time.perf_counter() - t_wall
+    ms_alpha = timed(lambda: S.acceptance_rate(li.target, li.draft, 1.0, alpha=alpha), args.steps)
+    ms_tail = timed(lambda: S.tail_stats(alpha, li.positions, lw.bin_tokens, lw.n_bins, 5.0),
+                    args.steps)
+    q, m, c = step()
+    torch.cuda.synchronize()
+    alg = T * 2 * V * esz                      # both logit rows of every token, read once
+    alg_tail = T * 8
+    dom_gbps = alg / (ms_alpha * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        n = 8
+        tg = li.target[:n].cpu() if lw.dtype == "f32" else None
+        rows_t = tg.numpy() if tg is not None else W.bf16_bits(li.target[:n])
+        rows_d = li.draft[:n].cpu().numpy() if lw.dtype == "f32" else W.bf16_bits(li.draft[:n])
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.acceptance(rows_t, rows_d)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds:
+                break
+        cpu = {"value": round(n * reps / el, 3), "unit": "tokens/s", "cores": oracle.num_threads(),
+               "kind": "oracle",
+               "sample": f"first {n} of {T} tokens of {lw.name}: fp64 acceptance rate over the "
+                         f"{V}-entry vocabulary, repeated {reps}x in {el:.1f} s"}
+    result = {
+        "metric": "acceptance rate tokens/sec (Eq. 1 over the full vocabulary) + per-bin "
+                  "5-percentile, achieved HBM GB/s (% of peak)",
+        "value": round(T / (ms_step * 1e-3), 2), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": lw.dtype, "data": "synthetic",
+        "config": {"workload": lw.name, "tokens": T, "vocab": V, "bin_tokens": lw.bin_tokens,
+                   "n_bins": lw.n_bins, "percentile": 5.0},
+        "achieved_GBps": round((alg + alg_tail) / (ms_step * 1e-3) / 1e9, 1),
+        "hbm_frac": round((alg + alg_tail) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "phase_ms": {"acceptance_rate": round(ms_alpha, 5), "tail_stats": round(ms_tail, 5)},
+        "roofline": {"kernel": f"k_acceptance<{'float' if esz == 4 else 'bf16'}>", "bound": "hbm",
+                     "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": acceptance_traffic(lw.name)},
+        "tail_5pct_per_bin": [round(float(x), 5) for x in q.cpu().numpy()],
+        "mean_per_bin": [round(float(x), 5) for x in m.cpu().numpy()],
+        "wall_s_timed": round(wall, 3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -203,6 +308,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.workload.startswith("a1"):
+        bench_acceptance(args)
         return
 
     import dataclasses

@@ -76,6 +76,9 @@ extern "C" {
 #define SPARROW_OUT_F32 0
 #define SPARROW_OUT_BF16 1
 
+#define SPARROW_LOGITS_F32 0
+#define SPARROW_LOGITS_BF16 1
+
 #define SPARROW_OP_SCORE_TOPK 0
 #define SPARROW_OP_SPARSE_ATTN 1
 #define SPARROW_OP_DENSE_ATTN 2
@@ -244,6 +247,65 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
                               const void *v_cache, const int32_t *block_table,
                               const int32_t *seq_lens, float scale, void *out, int32_t out_dtype,
                               void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Per-token acceptance rate between the dense policy and the sparse rollout
+ * (Sec. 3.1, Eq. 1: the expectation under the draft of min(p/q, 1), which equals
+ * the sum over the vocabulary of min(p(x), q(x))).
+ *
+ * For every token t < num_tokens, with a = target_logits[t][:] (dense policy) and
+ * b = draft_logits[t][:] (sparse rollout), rows of `vocab` entries:
+ *     p = softmax(inv_temperature * a),  q = softmax(inv_temperature * b),
+ *     alpha[t] = sum_x min(p(x), q(x))
+ * computed in fp32 (two passes: log-sum-exp of both rows, then the sum).  Agrees
+ * with an fp64 evaluation to about 1e-5.  logits_dtype is SPARROW_LOGITS_F32 or
+ * SPARROW_LOGITS_BF16; rows are contiguous ([num_tokens][vocab], row-major).
+ *
+ * Arguments: num_tokens >= 0; vocab >= 1; target_logits, draft_logits (device,
+ * element-aligned); inv_temperature finite; alpha (device fp32 [num_tokens],
+ * written); stream.
+ * Errors: SPARROW_EINVAL (null/misaligned pointer, bad size, non-finite
+ * temperature), SPARROW_EUNSUPPORTED (dtype), SPARROW_EHIP.
+ */
+int sparrow_acceptance_rate(int64_t num_tokens, int32_t vocab, int32_t logits_dtype,
+                            const void *target_logits, const void *draft_logits,
+                            float inv_temperature, float *alpha, void *stream);
+
+/*
+ * The approximation of the paper's measurement (Sec. 3.1, footnote: the inference
+ * engine returns the top-20 tokens and their log-probabilities per position):
+ *     alpha[t] = sum_{i < k} min(exp(lp_target[t][i]), exp(lp_draft[t][i]))
+ * over the k listed tokens, whose normalised log-probabilities under the two
+ * distributions are given (fp32 [num_tokens][k], device).  A lower bound of the
+ * exact rate.
+ * Errors: SPARROW_EINVAL (null/misaligned pointer, num_tokens < 0, k < 1), SPARROW_EHIP.
+ */
+int sparrow_acceptance_rate_topk(int64_t num_tokens, int32_t k, const float *lp_target,
+                                 const float *lp_draft, float *alpha, void *stream);
+
+/*
+ * Lower-tail statistic of the acceptance rate per length bin (Sec. 3.1 Method:
+ * the 5-percentile of the per-token rate; Sec. 3.2: tokens grouped by position
+ * in 2K-token bins).
+ *
+ * Token t (alpha[t], positions[t]) belongs to bin min(positions[t] / bin_tokens,
+ * n_bins - 1); tokens with a negative position are ignored.  For each bin b:
+ * count[b] = its number of tokens N, mean[b] = the fp64 mean of their alpha, and
+ * quantile[b] = the `percentile`-percentile with linear interpolation between
+ * order statistics: with the values sorted x_0 <= ... <= x_{N-1},
+ * h = (N - 1) * percentile / 100, lo = floor(h),
+ * quantile = x_lo + (h - lo) * (x_{lo+1} - x_lo)   (x_lo when lo = N - 1),
+ * in fp64.  Empty bins get count 0 and NaN mean and quantile.
+ *
+ * Arguments: num_tokens >= 0; alpha (device fp32), positions (device int32), both
+ * may be NULL when num_tokens is 0;
+ * bin_tokens >= 1; 1 <= n_bins <= 65535; 0 <= percentile <= 100; quantile,
+ * mean (device fp64 [n_bins]) and count (device int64 [n_bins]), written; stream.
+ * Errors: SPARROW_EINVAL, SPARROW_EHIP.
+ */
+int sparrow_tail_stats(int64_t num_tokens, const float *alpha, const int32_t *positions,
+                       int32_t bin_tokens, int32_t n_bins, double percentile, double *quantile,
+                       double *mean, int64_t *count, void *stream);
 
 /*
  * Workspace bytes needed by one call of `op` (SPARROW_OP_*) with this shape

@@ -16,7 +16,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsparrow.so")
-SOURCES = ["api.hip", "meta.hip", "append.hip", "score_topk.hip", "attention.hip"]
+SOURCES = ["api.hip", "meta.hip", "append.hip", "score_topk.hip", "attention.hip",
+           "acceptance.hip"]
 ARCH = "gfx950"
 # Packed fp32 VALU ops are switched off for every device compile.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

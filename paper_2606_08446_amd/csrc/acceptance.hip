@@ -1,0 +1,437 @@
+// Per-token acceptance rate between the dense policy and the sparse rollout (Sec. 3.1,
+// Eq. 1 of arXiv 2606.08446) and its lower-tail statistic per length bin (Sec. 3.1-3.2).
+//
+// k_acceptance: alpha_t = sum_x min(p(x), q(x)) with p, q the softmax of the target and draft
+// logit rows at inverse temperature tau.  One 1024-thread workgroup per token makes two
+// passes over its two rows: an online log-sum-exp of both (plain loads, so the rows stay in
+// the Infinity Cache for the second pass), then sum_x exp(min(tau a_x - P, tau b_x - Q)) -
+// one exp per vocabulary entry, since min(e^u, e^v) = e^min(u, v) - with non-temporal loads.
+// Rows are read as 16-byte vectors; a row that does not start 16-byte aligned is handled
+// with scalar head and tail elements.  Accumulation is fp32 per thread, tree reductions
+// across the workgroup.
+//
+// k_acceptance_topk: the approximation from the top-K listed tokens' normalised
+// log-probabilities, sum_i min(exp(lp_i), exp(lq_i)); one thread per token.
+//
+// k_tail_stats: one workgroup per position bin.  Count and fp64 sum of the bin's values,
+// then the order statistics x_lo and x_lo+1 (lo = floor((N - 1) pct / 100)) by a radix
+// select over order-preserving uint32 keys (8-bit digits, one scan of the tokens per
+// digit), and the percentile x_lo + (h - lo)(x_lo+1 - x_lo) in fp64 with the multiply and
+// the add rounded separately.
+#include "common.h"
+
+namespace sparrow {
+namespace {
+
+constexpr int kAccThreads = 1024;
+constexpr int kAccWaves = kAccThreads / 64;
+constexpr int kTailThreads = 1024;
+constexpr int kTailWaves = kTailThreads / 64;
+
+template <typename T> struct Logit;
+template <> struct Logit<float> {
+    static constexpr int kVec = 4;  // elements per 16-byte vector
+    __device__ static float at(const float *row, int64_t i) { return row[i]; }
+    __device__ static void unpack(u32x4_t v, float (&x)[kVec])
+    {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            x[e] = __uint_as_float(v[e]);
+    }
+};
+template <> struct Logit<uint16_t> {
+    static constexpr int kVec = 8;
+    __device__ static float at(const uint16_t *row, int64_t i)
+    {
+        return __uint_as_float((uint32_t)row[i] << 16);
+    }
+    __device__ static void unpack(u32x4_t v, float (&x)[kVec])
+    {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            x[2 * e] = bf16_lo(v[e]);
+            x[2 * e + 1] = bf16_hi(v[e]);
+        }
+    }
+};
+
+// Running (max, sum of exp(x - max)).
+struct Lse {
+    float m, s;
+};
+
+__device__ __forceinline__ Lse lse_merge(Lse a, Lse b)
+{
+    const float m = fmaxf(a.m, b.m);
+    if (m == -INFINITY)
+        return {m, 0.f};
+    return {m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
+}
+
+template <int N>
+__device__ __forceinline__ void lse_add(Lse &r, const float (&x)[N])
+{
+    float mx = x[0];
+#pragma unroll
+    for (int e = 1; e < N; ++e)
+        mx = fmaxf(mx, x[e]);
+    if (mx > r.m) {
+        r.s = r.m == -INFINITY ? 0.f : r.s * __expf(r.m - mx);
+        r.m = mx;
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+        s += __expf(x[e] - r.m);
+    r.s += s;
+}
+
+template <typename T>
+__device__ __forceinline__ void row_split(const T *row, int V, int &head, int &nvec)
+{
+    constexpr int W = Logit<T>::kVec;
+    const uintptr_t mis = reinterpret_cast<uintptr_t>(row) & 15u;
+    head = mis == 0 ? 0 : (int)((16u - mis) / sizeof(T));
+    if (head > V)
+        head = V;
+    nvec = (V - head) / W;
+}
+
+// Workgroup-wide reduction of a pair of Lse (target, draft) through LDS.
+__device__ void block_lse2(Lse &a, Lse &b, Lse (*s_red)[2])
+{
+#pragma unroll
+    for (int x = 1; x < 64; x <<= 1) {
+        a = lse_merge(a, {__shfl_xor(a.m, x, 64), __shfl_xor(a.s, x, 64)});
+        b = lse_merge(b, {__shfl_xor(b.m, x, 64), __shfl_xor(b.s, x, 64)});
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_red[wave][0] = a;
+        s_red[wave][1] = b;
+    }
+    __syncthreads();
+    a = s_red[0][0];
+    b = s_red[0][1];
+    for (int w = 1; w < kAccWaves; ++w) {
+        a = lse_merge(a, s_red[w][0]);
+        b = lse_merge(b, s_red[w][1]);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict__ target,
+                                                            const T *__restrict__ draft, int V,
+                                                            float tau, float *__restrict__ alpha)
+{
+    __shared__ Lse s_red[kAccWaves][2];
+    __shared__ float s_sum[kAccWaves];
+    constexpr int W = Logit<T>::kVec;
+    const int64_t t = blockIdx.x;
+    const T *pr = target + t * V;
+    const T *qr = draft + t * V;
+    const int tid = threadIdx.x;
+    int head, nvec;
+    row_split(pr, V, head, nvec);
+    const int tail0 = head + nvec * W;
+
+    // ---- pass 1: log-sum-exp of both rows
+    Lse a{-INFINITY, 0.f}, b{-INFINITY, 0.f};
+    for (int i = tid; i < head; i += kAccThreads) {
+        const float xa[1] = {tau * Logit<T>::at(pr, i)}, xb[1] = {tau * Logit<T>::at(qr, i)};
+        lse_add(a, xa);
+        lse_add(b, xb);
+    }
+    for (int i = tail0 + tid; i < V; i += kAccThreads) {
+        const float xa[1] = {tau * Logit<T>::at(pr, i)}, xb[1] = {tau * Logit<T>::at(qr, i)};
+        lse_add(a, xa);
+        lse_add(b, xb);
+    }
+    const u32x4_t *pv = reinterpret_cast<const u32x4_t *>(pr + head);
+    const u32x4_t *qv = reinterpret_cast<const u32x4_t *>(qr + head);
+    int v = tid;
+    for (; v + 3 * kAccThreads < nvec; v += 4 * kAccThreads) {
+        u32x4_t ra[4], rb[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            ra[u] = pv[v + u * kAccThreads];
+            rb[u] = qv[v + u * kAccThreads];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            float xa[W], xb[W];
+            Logit<T>::unpack(ra[u], xa);
+            Logit<T>::unpack(rb[u], xb);
+#pragma unroll
+            for (int e = 0; e < W; ++e) {
+                xa[e] *= tau;
+                xb[e] *= tau;
+            }
+            lse_add(a, xa);
+            lse_add(b, xb);
+        }
+    }
+    for (; v < nvec; v += kAccThreads) {
+        float xa[W], xb[W];
+        Logit<T>::unpack(pv[v], xa);
+        Logit<T>::unpack(qv[v], xb);
+#pragma unroll
+        for (int e = 0; e < W; ++e) {
+            xa[e] *= tau;
+            xb[e] *= tau;
+        }
+        lse_add(a, xa);
+        lse_add(b, xb);
+    }
+    block_lse2(a, b, s_red);
+    const float P = a.m + __logf(a.s);
+    const float Q = b.m + __logf(b.s);
+
+    // ---- pass 2: sum of exp(min(tau a - P, tau b - Q))
+    float acc = 0.f;
+    for (int i = tid; i < head; i += kAccThreads)
+        acc += __expf(fminf(tau * Logit<T>::at(pr, i) - P, tau * Logit<T>::at(qr, i) - Q));
+    for (int i = tail0 + tid; i < V; i += kAccThreads)
+        acc += __expf(fminf(tau * Logit<T>::at(pr, i) - P, tau * Logit<T>::at(qr, i) - Q));
+    v = tid;
+    for (; v + 3 * kAccThreads < nvec; v += 4 * kAccThreads) {
+        u32x4_t ra[4], rb[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            ra[u] = ld16_nt(pv + v + u * kAccThreads);
+            rb[u] = ld16_nt(qv + v + u * kAccThreads);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            float xa[W], xb[W];
+            Logit<T>::unpack(ra[u], xa);
+            Logit<T>::unpack(rb[u], xb);
+#pragma unroll
+            for (int e = 0; e < W; ++e)
+                acc += __expf(fminf(tau * xa[e] - P, tau * xb[e] - Q));
+        }
+    }
+    for (; v < nvec; v += kAccThreads) {
+        float xa[W], xb[W];
+        Logit<T>::unpack(pv[v], xa);
+        Logit<T>::unpack(qv[v], xb);
+#pragma unroll
+        for (int e = 0; e < W; ++e)
+            acc += __expf(fminf(tau * xa[e] - P, tau * xb[e] - Q));
+    }
+#pragma unroll
+    for (int x = 1; x < 64; x <<= 1)
+        acc += __shfl_xor(acc, x, 64);
+    if ((tid & 63) == 0)
+        s_sum[tid >> 6] = acc;
+    __syncthreads();
+    if (tid == 0) {
+        float total = 0.f;
+        for (int w = 0; w < kAccWaves; ++w)
+            total += s_sum[w];
+        alpha[t] = total;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_acceptance_topk(const float *__restrict__ lp_target,
+                                                         const float *__restrict__ lp_draft,
+                                                         int64_t T, int K,
+                                                         float *__restrict__ alpha)
+{
+    for (int64_t t = blockIdx.x * 256ll + threadIdx.x; t < T; t += (int64_t)gridDim.x * 256) {
+        float acc = 0.f;
+        for (int i = 0; i < K; ++i)
+            acc += __expf(fminf(lp_target[t * K + i], lp_draft[t * K + i]));
+        alpha[t] = acc;
+    }
+}
+
+// fp32 -> uint32 whose unsigned order is the order of the values (-0 == +0).
+__device__ __forceinline__ uint32_t float_key(float s)
+{
+    uint32_t u = __float_as_uint(s);
+    if (u == 0x80000000u)
+        u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float key_float(uint32_t k)
+{
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+__device__ __forceinline__ int bin_of(int32_t pos, int bin_tokens, int n_bins)
+{
+    if (pos < 0)
+        return -1;
+    const int b = pos / bin_tokens;
+    return b > n_bins - 1 ? n_bins - 1 : b;
+}
+
+// Exclusive-count radix select: the key of rank k (0-based) among the bin's keys.
+__device__ uint32_t select_rank(const float *alpha, const int32_t *pos, int64_t T, int bin,
+                                int bin_tokens, int n_bins, int64_t k, uint32_t *hist,
+                                int64_t *s_sel)
+{
+    uint32_t prefix = 0, mask = 0;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = threadIdx.x; i < 256; i += kTailThreads)
+            hist[i] = 0;
+        __syncthreads();
+        for (int64_t t = threadIdx.x; t < T; t += kTailThreads) {
+            if (bin_of(pos[t], bin_tokens, n_bins) != bin)
+                continue;
+            const uint32_t key = float_key(alpha[t]);
+            if ((key & mask) == prefix)
+                atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {  // 256 bins: a serial walk is short
+            int64_t below = 0;
+            int d = 0;
+            for (; d < 255; ++d) {
+                if (below + hist[d] > k)
+                    break;
+                below += hist[d];
+            }
+            s_sel[0] = d;
+            s_sel[1] = k - below;
+        }
+        __syncthreads();
+        prefix |= (uint32_t)s_sel[0] << shift;
+        mask |= 255u << shift;
+        k = s_sel[1];
+        __syncthreads();
+    }
+    return prefix;
+}
+
+__global__ __launch_bounds__(kTailThreads) void k_tail_stats(
+    const float *__restrict__ alpha, const int32_t *__restrict__ pos, int64_t T, int bin_tokens,
+    int n_bins, double pct, double *__restrict__ quantile, double *__restrict__ mean,
+    int64_t *__restrict__ count)
+{
+    __shared__ uint32_t hist[256];
+    __shared__ int64_t s_sel[2];
+    __shared__ double s_sum[kTailWaves];
+    __shared__ unsigned long long s_cnt[kTailWaves];
+    __shared__ uint32_t s_min;
+    const int bin = blockIdx.x;
+    double sum = 0.0;
+    unsigned long long n = 0;
+    for (int64_t t = threadIdx.x; t < T; t += kTailThreads) {
+        if (bin_of(pos[t], bin_tokens, n_bins) == bin) {
+            sum += (double)alpha[t];
+            ++n;
+        }
+    }
+#pragma unroll
+    for (int x = 1; x < 64; x <<= 1) {
+        sum += __shfl_xor(sum, x, 64);
+        n += __shfl_xor(n, x, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        s_sum[threadIdx.x >> 6] = sum;
+        s_cnt[threadIdx.x >> 6] = n;
+    }
+    __syncthreads();
+    double total = 0.0;
+    int64_t N = 0;
+    for (int w = 0; w < kTailWaves; ++w) {
+        total += s_sum[w];
+        N += (int64_t)s_cnt[w];
+    }
+    if (N == 0) {
+        if (threadIdx.x == 0) {
+            count[bin] = 0;
+            mean[bin] = __builtin_nan("");
+            quantile[bin] = __builtin_nan("");
+        }
+        return;
+    }
+    const double h = (double)(N - 1) * pct / 100.0;
+    int64_t lo = (int64_t)floor(h);
+    if (lo > N - 1)
+        lo = N - 1;
+    const uint32_t klo = select_rank(alpha, pos, T, bin, bin_tokens, n_bins, lo, hist, s_sel);
+    double x_hi;
+    const double x_lo = (double)key_float(klo);
+    if (lo + 1 >= N) {
+        x_hi = x_lo;
+    } else {
+        // rank lo + 1: x_lo again if enough keys equal it, else the smallest key above it
+        if (threadIdx.x == 0)
+            s_min = 0xffffffffu;
+        __syncthreads();
+        unsigned int le = 0;  // keys <= x_lo seen by this thread
+        uint32_t above = 0xffffffffu;
+        for (int64_t t = threadIdx.x; t < T; t += kTailThreads) {
+            if (bin_of(pos[t], bin_tokens, n_bins) != bin)
+                continue;
+            const uint32_t key = float_key(alpha[t]);
+            if (key <= klo)
+                ++le;
+            else if (key < above)
+                above = key;
+        }
+#pragma unroll
+        for (int x = 1; x < 64; x <<= 1) {
+            le += __shfl_xor(le, x, 64);
+            above = min(above, (uint32_t)__shfl_xor((int)above, x, 64));
+        }
+        if ((threadIdx.x & 63) == 0) {
+            s_cnt[threadIdx.x >> 6] = le;
+            atomicMin(&s_min, above);
+        }
+        __syncthreads();
+        int64_t n_le = 0;
+        for (int w = 0; w < kTailWaves; ++w)
+            n_le += (int64_t)s_cnt[w];
+        x_hi = n_le > lo + 1 ? x_lo : (double)key_float(s_min);
+    }
+    if (threadIdx.x == 0) {
+        // the definition's separate multiply and add (device code otherwise contracts to fma)
+#pragma clang fp contract(off)
+        count[bin] = N;
+        mean[bin] = total / (double)N;
+        quantile[bin] = x_lo + (h - (double)lo) * (x_hi - x_lo);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_acceptance(int64_t T, int V, int dtype, const void *target, const void *draft,
+                             float tau, float *alpha, hipStream_t stream)
+{
+    if (dtype == SPARROW_LOGITS_BF16)
+        hipLaunchKernelGGL(k_acceptance<uint16_t>, dim3((unsigned)T), dim3(kAccThreads), 0,
+                           stream, static_cast<const uint16_t *>(target),
+                           static_cast<const uint16_t *>(draft), V, tau, alpha);
+    else
+        hipLaunchKernelGGL(k_acceptance<float>, dim3((unsigned)T), dim3(kAccThreads), 0, stream,
+                           static_cast<const float *>(target), static_cast<const float *>(draft),
+                           V, tau, alpha);
+    return hipGetLastError();
+}
+
+hipError_t launch_acceptance_topk(int64_t T, int K, const float *lp_target, const float *lp_draft,
+                                  float *alpha, hipStream_t stream)
+{
+    int64_t blocks = (T + 255) / 256;
+    if (blocks > 65535)
+        blocks = 65535;
+    hipLaunchKernelGGL(k_acceptance_topk, dim3((unsigned)blocks), dim3(256), 0, stream, lp_target,
+                       lp_draft, T, K, alpha);
+    return hipGetLastError();
+}
+
+hipError_t launch_tail_stats(int64_t T, const float *alpha, const int32_t *pos, int bin_tokens,
+                             int n_bins, double pct, double *quantile, double *mean,
+                             int64_t *count, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_tail_stats, dim3(n_bins), dim3(kTailThreads), 0, stream, alpha, pos, T,
+                       bin_tokens, n_bins, pct, quantile, mean, count);
+    return hipGetLastError();
+}
+
+}  // namespace sparrow

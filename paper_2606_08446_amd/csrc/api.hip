@@ -1,5 +1,7 @@
 // C ABI of libsparrow: argument validation, workspace sizing and kernel launches.
 // Declarations and the contract of every entry point are in include/sparrow.h.
+#include <cmath>
+
 #include "common.h"
 
 using namespace sparrow;
@@ -192,6 +194,62 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
     return status_of(launch_attention(*shape, plan, q, k_cache, v_cache, block_table, seq_lens,
                                       nullptr, nullptr, 0, scale, out, out_dtype, workspace,
                                       static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_acceptance_rate(int64_t num_tokens, int32_t vocab, int32_t logits_dtype,
+                            const void *target_logits, const void *draft_logits,
+                            float inv_temperature, float *alpha, void *stream)
+{
+    if (num_tokens < 0 || vocab < 1 || !target_logits || !draft_logits || !alpha)
+        return SPARROW_EINVAL;
+    if (logits_dtype != SPARROW_LOGITS_F32 && logits_dtype != SPARROW_LOGITS_BF16)
+        return SPARROW_EUNSUPPORTED;
+    const uintptr_t esz = logits_dtype == SPARROW_LOGITS_BF16 ? 2 : 4;
+    if ((reinterpret_cast<uintptr_t>(target_logits) % esz) != 0 ||
+        (reinterpret_cast<uintptr_t>(draft_logits) % esz) != 0 || !al4(alpha))
+        return SPARROW_EINVAL;
+    // both rows of a token must share their alignment for the vector loads
+    if ((reinterpret_cast<uintptr_t>(target_logits) & 15u) !=
+        (reinterpret_cast<uintptr_t>(draft_logits) & 15u))
+        return SPARROW_EINVAL;
+    if (!std::isfinite(inv_temperature) || num_tokens > 0x7fffffff)
+        return SPARROW_EINVAL;
+    if (num_tokens == 0)
+        return SPARROW_OK;
+    return status_of(launch_acceptance(num_tokens, vocab, logits_dtype, target_logits,
+                                       draft_logits, inv_temperature, alpha,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_acceptance_rate_topk(int64_t num_tokens, int32_t k, const float *lp_target,
+                                 const float *lp_draft, float *alpha, void *stream)
+{
+    if (num_tokens < 0 || k < 1 || !lp_target || !lp_draft || !alpha)
+        return SPARROW_EINVAL;
+    if (!al4(lp_target) || !al4(lp_draft) || !al4(alpha))
+        return SPARROW_EINVAL;
+    if (num_tokens == 0)
+        return SPARROW_OK;
+    return status_of(launch_acceptance_topk(num_tokens, k, lp_target, lp_draft, alpha,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+int sparrow_tail_stats(int64_t num_tokens, const float *alpha, const int32_t *positions,
+                       int32_t bin_tokens, int32_t n_bins, double percentile, double *quantile,
+                       double *mean, int64_t *count, void *stream)
+{
+    if (num_tokens < 0 || bin_tokens < 1 || n_bins < 1 || n_bins > 65535)
+        return SPARROW_EINVAL;
+    if (!(percentile >= 0.0 && percentile <= 100.0))
+        return SPARROW_EINVAL;
+    if (!quantile || !mean || !count || (num_tokens > 0 && (!alpha || !positions)))
+        return SPARROW_EINVAL;
+    if (!al4(alpha) || !al4(positions) || (reinterpret_cast<uintptr_t>(quantile) & 7u) ||
+        (reinterpret_cast<uintptr_t>(mean) & 7u) || (reinterpret_cast<uintptr_t>(count) & 7u))
+        return SPARROW_EINVAL;
+    return status_of(launch_tail_stats(num_tokens, alpha, positions, bin_tokens, n_bins,
+                                       percentile, quantile, mean, count,
+                                       static_cast<hipStream_t>(stream)));
 }
 
 size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32_t op)

@@ -152,6 +152,14 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta
                              int32_t *out_idx, void *workspace, const AppendArgs &app,
                              hipStream_t stream);
 
+hipError_t launch_acceptance(int64_t T, int V, int dtype, const void *target, const void *draft,
+                             float tau, float *alpha, hipStream_t stream);
+hipError_t launch_acceptance_topk(int64_t T, int K, const float *lp_target, const float *lp_draft,
+                                  float *alpha, hipStream_t stream);
+hipError_t launch_tail_stats(int64_t T, const float *alpha, const int32_t *pos, int bin_tokens,
+                             int n_bins, double pct, double *quantile, double *mean,
+                             int64_t *count, hipStream_t stream);
+
 struct AttnPlan {
     size_t plan_bytes;       // page offsets and unit wave ranges at the start of the workspace
     size_t segments;         // partial-result slots (waves + units)

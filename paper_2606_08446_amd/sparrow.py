@@ -30,12 +30,15 @@ SPARROW_MAX_PAGES_PER_SEQ = 15360
 SPARROW_MAX_BATCH = 8192
 SPARROW_OUT_F32 = 0
 SPARROW_OUT_BF16 = 1
+SPARROW_LOGITS_F32 = 0
+SPARROW_LOGITS_BF16 = 1
 SPARROW_OP_SCORE_TOPK = 0
 SPARROW_OP_SPARSE_ATTN = 1
 SPARROW_OP_DENSE_ATTN = 2
 
 EXPORTS = ("sparrow_page_meta_update", "sparrow_append_kv", "sparrow_page_score_topk",
            "sparrow_append_score_topk", "sparrow_sparse_decode_attn", "sparrow_dense_decode_attn",
+           "sparrow_acceptance_rate", "sparrow_acceptance_rate_topk", "sparrow_tail_stats",
            "sparrow_workspace_size", "sparrow_status_string")
 
 
@@ -84,7 +87,12 @@ def load():
     lib.sparrow_append_score_topk.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _p,
                                               ctypes.POINTER(Schedule), _i32, _p, _p, _p,
                                               ctypes.c_size_t, _p]
-    for fn in EXPORTS[:6]:
+    lib.sparrow_acceptance_rate.argtypes = [ctypes.c_int64, _i32, _i32, _p, _p, ctypes.c_float,
+                                            _p, _p]
+    lib.sparrow_acceptance_rate_topk.argtypes = [ctypes.c_int64, _i32, _p, _p, _p, _p]
+    lib.sparrow_tail_stats.argtypes = [ctypes.c_int64, _p, _p, _i32, _i32, ctypes.c_double, _p,
+                                       _p, _p, _p]
+    for fn in EXPORTS[:9]:
         getattr(lib, fn).restype = ctypes.c_int
     lib.sparrow_workspace_size.argtypes = [sp, _i32, _i32]
     lib.sparrow_workspace_size.restype = ctypes.c_size_t
@@ -133,6 +141,22 @@ def sparrow_dense_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens,
     return load().sparrow_dense_decode_attn(ctypes.byref(shape), q, k_cache, v_cache,
                                             block_table, seq_lens, scale, out, out_dtype,
                                             workspace, ws_bytes, stream)
+
+
+def sparrow_acceptance_rate(num_tokens, vocab, logits_dtype, target, draft, inv_temperature,
+                            alpha, stream):
+    return load().sparrow_acceptance_rate(num_tokens, vocab, logits_dtype, target, draft,
+                                          inv_temperature, alpha, stream)
+
+
+def sparrow_acceptance_rate_topk(num_tokens, k, lp_target, lp_draft, alpha, stream):
+    return load().sparrow_acceptance_rate_topk(num_tokens, k, lp_target, lp_draft, alpha, stream)
+
+
+def sparrow_tail_stats(num_tokens, alpha, positions, bin_tokens, n_bins, percentile, quantile,
+                       mean, count, stream):
+    return load().sparrow_tail_stats(num_tokens, alpha, positions, bin_tokens, n_bins, percentile,
+                                     quantile, mean, count, stream)
 
 
 def sparrow_workspace_size(shape, k_max, op) -> int:
@@ -291,6 +315,51 @@ def dense_decode_attn(q, k_cache, v_cache, block_table, seq_lens, scale=None, ou
                                    _stream(q.device))
     _check("sparrow_dense_decode_attn", rc)
     return out
+
+
+def acceptance_rate(target, draft, inv_temperature=1.0, alpha=None):
+    """Per-token acceptance rate of logit rows ``[T][V]`` (float32 or bfloat16, same dtype).
+    Returns alpha fp32 ``[T]``."""
+    import torch
+    _require_device(target)
+    if target.dtype != draft.dtype or target.shape != draft.shape:
+        raise ValueError("target and draft logits need the same dtype and shape")
+    dt = {torch.float32: SPARROW_LOGITS_F32, torch.bfloat16: SPARROW_LOGITS_BF16}[target.dtype]
+    T, V = target.shape
+    if not (target.is_contiguous() and draft.is_contiguous()):
+        raise ValueError("logit rows must be contiguous")
+    if alpha is None:
+        alpha = torch.empty(T, dtype=torch.float32, device=target.device)
+    _check("sparrow_acceptance_rate", sparrow_acceptance_rate(
+        T, V, dt, _ptr(target), _ptr(draft), float(inv_temperature), _ptr(alpha),
+        _stream(target.device)))
+    return alpha
+
+
+def acceptance_rate_topk(lp_target, lp_draft, alpha=None):
+    """Top-K approximation from log-probabilities ``[T][K]`` (fp32).  Returns alpha ``[T]``."""
+    import torch
+    _require_device(lp_target)
+    T, K = lp_target.shape
+    if alpha is None:
+        alpha = torch.empty(T, dtype=torch.float32, device=lp_target.device)
+    _check("sparrow_acceptance_rate_topk", sparrow_acceptance_rate_topk(
+        T, K, _ptr(lp_target), _ptr(lp_draft), _ptr(alpha), _stream(lp_target.device)))
+    return alpha
+
+
+def tail_stats(alpha, positions, bin_tokens, n_bins, percentile=5.0):
+    """(quantile fp64 [n_bins], mean fp64 [n_bins], count int64 [n_bins]) on the device."""
+    import torch
+    _require_device(alpha)
+    dev = alpha.device
+    q = torch.empty(n_bins, dtype=torch.float64, device=dev)
+    m = torch.empty(n_bins, dtype=torch.float64, device=dev)
+    c = torch.empty(n_bins, dtype=torch.int64, device=dev)
+    _check("sparrow_tail_stats", sparrow_tail_stats(
+        alpha.numel(), _ptr(alpha), _ptr(positions), int(bin_tokens), int(n_bins),
+        float(percentile), _ptr(q), _ptr(m), _ptr(c), _stream(dev)))
+    return q, m, c
 
 
 class SparseDecodeStep:

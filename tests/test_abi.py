@@ -224,3 +224,43 @@ def test_misaligned_pointers_are_rejected(lib, fn, arg):
 @pytest.mark.parametrize("fn,arg", [(f, a) for f, args in VEC16.items() for a in args])
 def test_vector_pointers_need_16_byte_alignment(lib, fn, arg):
     assert call(fn, good_shape(), **{arg: FAKE + 4}) == S.SPARROW_EINVAL
+
+
+def test_acceptance_entry_points_validate_arguments(lib):
+    f32, bf16 = S.SPARROW_LOGITS_F32, S.SPARROW_LOGITS_BF16
+    ok = dict(n=4, v=100, dt=f32, t=FAKE, d=FAKE, tau=1.0, a=FAKE)
+
+    def acc(**kw):
+        a = dict(ok, **kw)
+        return S.sparrow_acceptance_rate(a["n"], a["v"], a["dt"], a["t"], a["d"], a["tau"],
+                                         a["a"], None)
+    assert acc(n=0) == S.SPARROW_OK
+    assert acc(n=-1) == S.SPARROW_EINVAL
+    assert acc(v=0) == S.SPARROW_EINVAL
+    assert acc(dt=5) == S.SPARROW_EUNSUPPORTED
+    for arg in ("t", "d", "a"):
+        assert acc(**{arg: None}) == S.SPARROW_EINVAL
+    assert acc(t=FAKE + 2) == S.SPARROW_EINVAL                 # fp32 rows need 4-byte alignment
+    assert acc(dt=bf16, t=FAKE + 2, d=FAKE + 18, n=0) == S.SPARROW_OK   # same 16-byte phase
+    assert acc(dt=bf16, t=FAKE + 2, d=FAKE + 4) == S.SPARROW_EINVAL     # different phases
+    assert acc(tau=float("nan")) == S.SPARROW_EINVAL
+    assert acc(tau=float("inf")) == S.SPARROW_EINVAL
+    assert S.sparrow_acceptance_rate_topk(0, 20, FAKE, FAKE, FAKE, None) == S.SPARROW_OK
+    assert S.sparrow_acceptance_rate_topk(5, 0, FAKE, FAKE, FAKE, None) == S.SPARROW_EINVAL
+    assert S.sparrow_acceptance_rate_topk(5, 20, None, FAKE, FAKE, None) == S.SPARROW_EINVAL
+    assert S.sparrow_acceptance_rate_topk(5, 20, FAKE + 2, FAKE, FAKE, None) == S.SPARROW_EINVAL
+
+    def tail(**kw):
+        a = dict(n=10, al=FAKE, pos=FAKE, bt=2048, nb=20, pct=5.0, q=FAKE, m=FAKE, c=FAKE)
+        a.update(kw)
+        return S.sparrow_tail_stats(a["n"], a["al"], a["pos"], a["bt"], a["nb"], a["pct"],
+                                    a["q"], a["m"], a["c"], None)
+    assert tail(n=-1) == S.SPARROW_EINVAL
+    assert tail(bt=0) == S.SPARROW_EINVAL
+    assert tail(nb=0) == S.SPARROW_EINVAL and tail(nb=65536) == S.SPARROW_EINVAL
+    assert tail(pct=-0.5) == S.SPARROW_EINVAL and tail(pct=100.5) == S.SPARROW_EINVAL
+    assert tail(pct=float("nan")) == S.SPARROW_EINVAL
+    for arg in ("al", "pos", "q", "m", "c"):
+        assert tail(**{arg: None}) == S.SPARROW_EINVAL
+    assert tail(n=0, q=None) == S.SPARROW_EINVAL
+    assert tail(q=FAKE + 4) == S.SPARROW_EINVAL               # fp64 outputs need 8-byte alignment

@@ -1,0 +1,133 @@
+"""GPU parity of the acceptance-rate kernels (Sec. 3.1, Eq. 1) and of the per-bin tail
+statistic, through the C ABI, against the CPU oracle.
+
+Tolerance of alpha: 2e-5 absolute.  The kernel works in fp32: per-element exp and the
+(tau * logit - LSE) difference carry relative errors of a few 1e-7 (|logits| <= ~30), the
+log-sum-exp of a row about 1e-6; each perturbs alpha (a sum of at most 1) by a few 1e-6.
+The tail statistic is checked on the GPU's own fp32 alpha on both sides: counts and the
+quantile (an order statistic and one fp64 interpolation) bit-exact, the mean to 1e-12
+relative (fp64 sums in a different order)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_08446_amd import sparrow as S
+from paper_2606_08446_amd import workloads as W
+
+from parity import log
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+ALPHA_TOL = 2e-5
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu(gpu_device):
+    S.load()
+    yield
+
+
+def host_rows(t):
+    if t.dtype == torch.bfloat16:
+        return W.bf16_bits(t)
+    return t.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V,tau", [(3000, 1.0), (3001, 1.0), (4099, 0.7), (1, 1.0), (12, 0.0)])
+def test_acceptance_matches_oracle(dtype, V, tau):
+    log(f"case acceptance {dtype} V={V} tau={tau}")
+    li = W.generate_logits(W.small_logits(T=37, V=V, seed=3, dtype=dtype), DEV)
+    got = S.acceptance_rate(li.target, li.draft, tau)
+    torch.cuda.synchronize()
+    ref = oracle.acceptance(host_rows(li.target), host_rows(li.draft), tau)
+    err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+    log(f"  max abs err {err.max():.2e}")
+    assert err.max() <= ALPHA_TOL
+    if V == 1 or tau == 0.0:
+        np.testing.assert_allclose(got.cpu().numpy(), 1.0, rtol=0, atol=2e-6)
+
+
+def test_acceptance_unaligned_row_starts():
+    # views whose rows start off a 16-byte boundary (both rows in the same phase)
+    li = W.generate_logits(W.small_logits(T=9, V=2051, seed=4), DEV)
+    for off in (1, 2, 3):
+        t = li.target.view(-1)[off:off + 8 * 2051].view(8, 2051)
+        d = li.draft.view(-1)[off:off + 8 * 2051].view(8, 2051)
+        got = S.acceptance_rate(t, d)
+        torch.cuda.synchronize()
+        ref = oracle.acceptance(t.cpu().numpy(), d.cpu().numpy())
+        assert np.abs(got.cpu().numpy() - ref).max() <= ALPHA_TOL, off
+
+
+def test_acceptance_topk_matches_oracle():
+    rng = np.random.default_rng(6)
+    T, K = 1000, 20
+    lp = np.log(rng.dirichlet(np.ones(K) * 0.3, size=T) * 0.97).astype(np.float32)
+    lq = np.log(rng.dirichlet(np.ones(K) * 0.3, size=T) * 0.97).astype(np.float32)
+    got = S.acceptance_rate_topk(torch.as_tensor(lp, device=DEV), torch.as_tensor(lq, device=DEV))
+    torch.cuda.synchronize()
+    ref = oracle.acceptance_topk(lp, lq)
+    assert np.abs(got.cpu().numpy() - ref).max() <= 1e-6
+
+
+def tail_case(alpha, pos, bin_tokens, n_bins, pct):
+    a = torch.as_tensor(alpha, device=DEV)
+    p = torch.as_tensor(pos, device=DEV)
+    q, m, c = S.tail_stats(a, p, bin_tokens, n_bins, pct)
+    torch.cuda.synchronize()
+    rq, rm, rc = oracle.tail_stats(alpha, pos, bin_tokens, n_bins, pct)
+    np.testing.assert_array_equal(c.cpu().numpy(), rc)
+    np.testing.assert_array_equal(q.cpu().numpy(), rq)          # NaN == NaN for empty bins
+    gm = m.cpu().numpy()
+    ok = rc > 0
+    np.testing.assert_allclose(gm[ok], rm[ok], rtol=1e-12, atol=0)
+    assert np.isnan(gm[~ok]).all()
+
+
+@pytest.mark.parametrize("pct", [0.0, 5.0, 12.5, 50.0, 100.0])
+def test_tail_stats_match_oracle(pct):
+    log(f"case tail stats pct={pct}")
+    rng = np.random.default_rng(7)
+    T = 20000
+    alpha = (1.0 - rng.beta(0.3, 4.0, size=T) * 0.7).astype(np.float32)
+    alpha[::7] = np.float32(1.0)                     # many exact ties
+    alpha[3::11] = np.round(alpha[3::11], 2)
+    pos = rng.integers(-100, 50000, size=T).astype(np.int32)   # negatives, past the last bin
+    pos[(pos >= 6144) & (pos < 8192)] = 9000                   # bin 3 empty
+    tail_case(alpha, pos, 2048, 20, pct)
+
+
+def test_tail_stats_small_and_degenerate():
+    tail_case(np.array([0.25], np.float32), np.array([5], np.int32), 2048, 3, 5.0)
+    tail_case(np.array([0.5, 0.5, 0.5, 0.5], np.float32), np.array([0, 1, 2, 3], np.int32),
+              2048, 1, 5.0)
+    tail_case(np.array([0.0, -0.0, 1.0], np.float32), np.array([0, 1, 2], np.int32), 2048, 1, 50.0)
+    tail_case(np.zeros(0, np.float32), np.zeros(0, np.int32), 2048, 4, 5.0)
+
+
+@pytest.mark.parametrize("cfg", ["a1", "a1-bf16"])
+def test_full_size_acceptance_and_tail(cfg):
+    lw = W.LOGIT_CONFIGS[cfg]
+    log(f"case full-size {lw.name}")
+    li = W.generate_logits(lw, DEV)
+    alpha = S.acceptance_rate(li.target, li.draft)
+    q, m, c = S.tail_stats(alpha, li.positions, lw.bin_tokens, lw.n_bins, 5.0)
+    torch.cuda.synchronize()
+    a = alpha.cpu().numpy()
+    rng = np.random.default_rng(8)
+    sample = np.sort(rng.choice(lw.tokens, size=48, replace=False))
+    sel = torch.as_tensor(sample, device=DEV)
+    ref = oracle.acceptance(host_rows(li.target[sel]), host_rows(li.draft[sel]))
+    err = np.abs(a[sample].astype(np.float64) - ref)
+    log(f"  sampled alpha max abs err {err.max():.2e}")
+    assert err.max() <= ALPHA_TOL
+    rq, rm, rc = oracle.tail_stats(a, li.positions.cpu().numpy(), lw.bin_tokens, lw.n_bins, 5.0)
+    np.testing.assert_array_equal(c.cpu().numpy(), rc)
+    np.testing.assert_array_equal(q.cpu().numpy(), rq)
+    np.testing.assert_allclose(m.cpu().numpy(), rm, rtol=1e-12)
+    log(f"  5-percentile per bin: {np.round(rq, 4).tolist()}")
+    del li
+    torch.cuda.empty_cache()
