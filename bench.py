@@ -39,8 +39,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c2",
-                    help="c1..c5, or c4-2/c4-5/c4-10/c4-25/c4-100; a1 / a1-bf16 for the "
-                         "acceptance rate over paired logit rows")
+                    help="c1..c5, or c4-2/c4-5/c4-10/c4-25/c4-100; t4-<page size>-<16k|24k|32k>"
+                         "[-b<batch>] for the page-size study; a1 / a1-bf16 for the acceptance "
+                         "rate over paired logit rows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample")
@@ -59,6 +60,10 @@ def parse():
 
 def workload(name):
     from paper_2606_08446_amd import workloads as W
+    if name.startswith("t4-"):   # t4-<page size>-<past tokens in K>[-b<batch>]
+        parts = name.split("-")
+        batch = int(parts[3][1:]) if len(parts) > 3 else 16
+        return W.table4(int(parts[1]), int(parts[2].rstrip("k")) * 1024, batch)
     if name.startswith("c4-"):
         pct = {"2": 0, "5": 1, "10": 2, "25": 3, "100": 4}[name.split("-")[1]]
         return W.c4_with_fraction(pct)
@@ -479,6 +484,8 @@ def main():
         cpu = cpu_baseline(inp, lens_last, lay0.k_new[len(lens_host_steps) - 1],
                            lay0.v_new[len(lens_host_steps) - 1], k_max, args.cpu_seconds)
 
+    from paper_2606_08446_amd import cost_model
+    d_el, s_el = cost_model.decode_step_elements(lens_last, np.asarray(k_host) * ps, ps, Hkv * 128)
     budgets = np.asarray(k_host)
     kernels = {"sparse_attn": "k_attn_stream<sparse> + k_attn_merge",
                "append_score_topk": "k_page_score (with append) + k_topk",
@@ -515,6 +522,8 @@ def main():
                   "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4),
                   "step": "append, dense attention"},
         "speedup_vs_dense": round(ms_dense / ms_step, 3),
+        "cost_model": {"dense_elements": int(d_el), "sparse_elements": int(s_el),
+                       "predicted_speedup_memory_bound": round(d_el / s_el, 3)},
         "roofline": {"kernel": kernels[dominant],
                      "bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),

@@ -123,6 +123,16 @@ C5 = Workload("c5_qwen3_14b_b64", 64, 40, 8, 16, 32768, 65536, 15,
 CONFIGS = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5}
 
 
+def table4(page_size: int, length: int, batch: int = 16) -> Workload:
+    """The page-size study of Table 4: a Qwen3-1.7B-shaped layer (16/8 heads), ``batch``
+    sequences of ``length`` past tokens, a fixed budget of 1024 tokens (1024 / page_size
+    pages)."""
+    return Workload(f"t4_ps{page_size}_l{length // 1024}k_b{batch}", batch, 16, 8, page_size,
+                    length, length, 16, fixed_budget(1024 // page_size),
+                    description=f"Table 4 page-size study: {page_size}-token pages x "
+                                f"{1024 // page_size}, {length} past tokens, batch {batch}")
+
+
 def c4_with_fraction(i: int) -> Workload:
     num, den = C4_FRACTIONS[i]
     return dataclasses.replace(C4, schedule=fraction_budget(num, den),
