@@ -59,6 +59,13 @@ def _load():
     lib.oracle_tail_stats.argtypes = [ctypes.c_int64, _p, _p, _i32, _i32, ctypes.c_double, _p, _p,
                                       _p]
     lib.oracle_tail_stats.restype = None
+    lib.oracle_page_key_sums.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p]
+    lib.oracle_page_key_sums.restype = None
+    lib.oracle_page_scores_mean.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p,
+                                            _p, _p]
+    lib.oracle_page_scores_mean.restype = None
+    lib.oracle_select_forced.argtypes = [_i32, _i32, _i32, _i32, _p, _p, _p, _i32, _i32, _i32, _p]
+    lib.oracle_select_forced.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = _i32
     _lib = lib
@@ -112,10 +119,23 @@ def page_meta(k_cache, block_table, seq_lens, first_pos=None, meta=None) -> np.n
     return out
 
 
-def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta, inplace=False):
+def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta, inplace=False,
+              landmark="minmax"):
     """(k_cache, v_cache, meta) after writing token ``L_b - 1`` of every sequence (rows
     ``k_new``/``v_new`` ``[B][Hkv][D]``) and rebuilding the metadata of its page: copies, or
-    the given arrays updated in place (C-contiguous uint16) with ``inplace``."""
+    the given arrays updated in place (C-contiguous uint16) with ``inplace``.  With
+    ``landmark="mean"`` ``meta`` is the fp32 key-sum array ``[P][Hkv][D]``."""
+    if landmark == "mean":
+        P, Hkv, ps, D = k_cache.shape
+        scratch = np.zeros((P, Hkv, 2, D), np.uint16)
+        kc, vc, _ = append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, scratch,
+                              inplace=inplace)
+        lens = np.asarray(seq_lens, np.int32)
+        first = np.where((lens >= 1) & (lens <= ps * block_table.shape[1]), lens - 1,
+                         np.iinfo(np.int32).max).astype(np.int32)
+        sums = page_key_sums(kc, block_table, np.minimum(lens, ps * block_table.shape[1]),
+                             first_pos=first, sums=meta, inplace=inplace)
+        return kc, vc, sums
     P, Hkv, ps, D = k_cache.shape
     B, max_pages = block_table.shape
     kn, knp = _c(k_new, np.uint16)
@@ -256,3 +276,55 @@ def tail_stats(alpha, positions, bin_tokens, n_bins, pct):
     _load().oracle_tail_stats(len(a), ap, pp, int(bin_tokens), int(n_bins), float(pct),
                               q.ctypes.data, m.ctypes.data, c.ctypes.data)
     return q, m, c
+
+
+# ----------------------------------------------------------------- selector variants
+def page_key_sums(k_cache, block_table, seq_lens, first_pos=None, sums=None, inplace=False):
+    """Mean-landmark metadata: fp32 key sums ``[P][Hkv][D]`` of the pages overlapping
+    ``[first_pos[b], L_b)`` (all pages without ``first_pos``), updated in a copy of ``sums``
+    (or in place)."""
+    P, Hkv, ps, D = k_cache.shape
+    B, max_pages = block_table.shape
+    kc, kcp = _c(k_cache, np.uint16)
+    bt, btp = _c(block_table, np.int32)
+    sl, slp = _c(seq_lens, np.int32)
+    if sums is None:
+        out = np.zeros((P, Hkv, D), np.float32)
+    elif inplace:
+        if sums.dtype != np.float32 or not sums.flags.c_contiguous:
+            raise ValueError("in-place update needs a C-contiguous float32 array")
+        out = sums
+    else:
+        out = np.array(sums, dtype=np.float32, copy=True, order="C")
+    fp_arr, fpp = (None, None) if first_pos is None else _c(first_pos, np.int32)
+    _load().oracle_page_key_sums(B, Hkv, D, ps, max_pages, kcp, btp, slp, fpp, out.ctypes.data)
+    return out
+
+
+def page_scores_mean(q, sums, block_table, seq_lens, ps):
+    """Mean-landmark page scores (scores32, scores64), each ``[B][Hkv][max_pages]``."""
+    B, Hq, D = q.shape
+    P, Hkv, _ = sums.shape
+    max_pages = block_table.shape[1]
+    qq, qp = _c(q, np.uint16)
+    ss, sp_ = _c(sums, np.float32)
+    bt, btp = _c(block_table, np.int32)
+    sl, slp = _c(seq_lens, np.int32)
+    s32 = np.full((B, Hkv, max_pages), np.nan, np.float32)
+    s64 = np.full((B, Hkv, max_pages), np.nan, np.float64)
+    _load().oracle_page_scores_mean(B, Hq, Hkv, D, ps, max_pages, qp, sp_, btp, slp,
+                                    s32.ctypes.data, s64.ctypes.data)
+    return s32, s64
+
+
+def select_forced(seq_lens, k_of_seq, scores32, ps, k_max, sink, local) -> np.ndarray:
+    """Top-k page lists with pages ``[0, sink)`` and ``[n - local, n)`` forced first."""
+    B, Hkv, max_pages = scores32.shape
+    sl, slp = _c(seq_lens, np.int32)
+    kk, kp = _c(k_of_seq, np.int32)
+    sc, scp = _c(scores32, np.float32)
+    out = np.zeros((B, Hkv, k_max), np.int32)
+    _load().oracle_select_forced(B, Hkv, ps, max_pages, slp, kp, scp, int(sink), int(local),
+                                 int(k_max), out.ctypes.data)
+    return out
+

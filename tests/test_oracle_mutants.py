@@ -13,7 +13,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 ORACLE = os.path.join(ROOT, "oracle")
-SOURCES = ("sparrow_oracle.c", "acceptance_oracle.c")
+SOURCES = ("sparrow_oracle.c", "acceptance_oracle.c", "selector_oracle.c")
 
 MUTANTS = {
     "topk_ties_to_higher_index": ("return (a->p > b->p) - (a->p < b->p);",
@@ -60,9 +60,25 @@ ACCEPTANCE_MUTANTS = {
     "tail_bin_not_clamped": ("            if (bin > n_bins - 1)\n                bin = n_bins - 1;",
                              "            if (bin > n_bins)\n                bin = n_bins - 1;"),
 }
+# Mistakes in the selector-variant oracle, pinned by test_oracle_selector.py.
+SELECTOR_MUTANTS = {
+    "mean_divides_by_page_size": ("s32 += bf16f(qj[i]) * (sm[i] / (float)valid);",
+                                  "s32 += bf16f(qj[i]) * (sm[i] / (float)ps);"),
+    "mean64_divides_by_page_size": (
+        "s64 += (double)bf16f(qj[i]) * ((double)sm[i] / (double)valid);",
+        "s64 += (double)bf16f(qj[i]) * ((double)sm[i] / (double)ps);"),
+    "key_sums_skip_last_token": ("for (int64_t t = 0; t < valid; ++t)\n                        s +=",
+                                 "for (int64_t t = 0; t < valid - 1; ++t)\n                        s +="),
+    "forced_ignores_local_pages": ("r[p].forced = (p < sink || p >= n - local) ? 0 : 1;",
+                                   "r[p].forced = (p < sink) ? 0 : 1;"),
+    "forced_ties_to_higher_index": ("return (a->p > b->p) - (a->p < b->p);",
+                                    "return (a->p < b->p) - (a->p > b->p);"),
+}
 CASES = [(n, "sparrow_oracle.c", o, w, "test_oracle.py") for n, (o, w) in MUTANTS.items()] + \
         [(n, "acceptance_oracle.c", o, w, "test_oracle_acceptance.py")
-         for n, (o, w) in ACCEPTANCE_MUTANTS.items()]
+         for n, (o, w) in ACCEPTANCE_MUTANTS.items()] + \
+        [(n, "selector_oracle.c", o, w, "test_oracle_selector.py")
+         for n, (o, w) in SELECTOR_MUTANTS.items()]
 
 
 @pytest.mark.parametrize("name,fname,old,new,pins", sorted(CASES), ids=[c[0] for c in sorted(CASES)])
