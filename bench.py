@@ -48,6 +48,10 @@ def parse():
     ap.add_argument("--step", choices=("fused", "separate"), default="fused",
                     help="fused: sparrow_append_score_topk + attention; separate: "
                          "sparrow_append_kv, sparrow_page_score_topk, attention")
+    ap.add_argument("--landmark", choices=("minmax", "mean"), default="minmax",
+                    help="page landmark: channel-wise key min/max (default) or mean key")
+    ap.add_argument("--sink", type=int, default=0, help="forced sink pages [0, s)")
+    ap.add_argument("--local", type=int, default=0, help="forced most recent pages")
     ap.add_argument("--layers", type=int, default=1,
                     help="attention layers per step, each with its own cache (value stays per "
                          "layer: batch x layers / step time)")
@@ -338,6 +342,7 @@ def main():
     B, Hkv = w.batch, w.num_kv_heads
     total = Wm + K
     fused = args.step == "fused"
+    landmark = S.SPARROW_LANDMARK_MEAN if args.landmark == "mean" else S.SPARROW_LANDMARK_MINMAX
 
     class Layer:
         """One attention layer: its own cache, metadata and new rows; the lengths (and so
@@ -355,12 +360,13 @@ def main():
             self.v_new = torch.randn((total, B, Hkv, 128), generator=gen,
                                      device=dev).to(torch.bfloat16)
             inp = self.inp
-            self.meta = torch.zeros((inp.num_phys_pages, Hkv, 2, 128), dtype=torch.bfloat16,
-                                    device=dev)
-            S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, self.meta)
+            self.meta = S.new_meta(inp.num_phys_pages, Hkv, dev, landmark)
+            S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, self.meta,
+                               landmark=landmark)
             self.step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table,
                                            inp.seq_lens, self.meta, inp.min_pages, inp.frac_num,
-                                           s.frac_den, s.bin_tokens, k_max)
+                                           s.frac_den, s.bin_tokens, k_max, landmark=landmark,
+                                           sink_pages=args.sink, local_pages=args.local)
             self.dense_out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
             self.dense_ws = torch.empty(max(16, S.sparrow_workspace_size(
                 self.step.shape, 0, S.SPARROW_OP_DENSE_ATTN)), dtype=torch.uint8, device=dev)
@@ -507,7 +513,8 @@ def main():
                    "num_kv_heads": Hkv, "head_dim": 128, "page_size": ps,
                    "len_range": [w.len_lo, w.len_hi], "budget_pages": [int(budgets.min()),
                                                                        int(budgets.max())],
-                   "k_max": int(k_max), "layers": L_layers,
+                   "k_max": int(k_max), "layers": L_layers, "landmark": args.landmark,
+                   "sink_pages": args.sink, "local_pages": args.local,
                    "graph": bool(args.graph),
                    "step": ("append+score+top-k fused, attention" if fused else
                             "append, score+top-k, attention") +

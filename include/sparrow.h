@@ -39,7 +39,10 @@
  *      k_cache      bf16  [num_phys_pages][num_kv_heads][page_size][head_dim]
  *      v_cache      bf16  [num_phys_pages][num_kv_heads][page_size][head_dim]
  *      meta         bf16  [num_phys_pages][num_kv_heads][2][head_dim]
- *                         (row 0: channel-wise min, row 1: channel-wise max)
+ *                         (row 0: channel-wise min, row 1: channel-wise max), or with
+ *                         SPARROW_LANDMARK_MEAN fp32 [num_phys_pages][num_kv_heads][head_dim]
+ *                         (channel-wise sum of the page's valid keys) - 512 B per
+ *                         (page, head) either way
  *      block_table  int32 [batch][max_pages_per_seq]  logical -> physical page
  *      seq_lens     int32 [batch]  tokens of each sequence, including the token
  *                                  being decoded (0 allowed)
@@ -49,6 +52,7 @@
  *    only those block-table entries are read.  Query head j reads KV head
  *    j / G with G = num_q_heads / num_kv_heads (grouped-query attention).
  *  - Supported shapes: head_dim == 128; page_size in {16, 32, 64, 128};
+ *    landmark in {SPARROW_LANDMARK_MINMAX, SPARROW_LANDMARK_MEAN};
  *    num_q_heads a multiple of num_kv_heads with G <= 16;
  *    1 <= max_pages_per_seq <= SPARROW_MAX_PAGES_PER_SEQ;
  *    batch * num_kv_heads <= 65535; batch <= SPARROW_MAX_BATCH for the
@@ -76,6 +80,10 @@ extern "C" {
 #define SPARROW_OUT_F32 0
 #define SPARROW_OUT_BF16 1
 
+#define SPARROW_LANDMARK_MINMAX 0 /* per page: channel-wise min and max of the keys (bf16)  */
+#define SPARROW_LANDMARK_MEAN 1   /* per page: channel-wise sum of the keys (fp32); scored
+                                     as the mean key                                       */
+
 #define SPARROW_LOGITS_F32 0
 #define SPARROW_LOGITS_BF16 1
 
@@ -83,7 +91,9 @@ extern "C" {
 #define SPARROW_OP_SPARSE_ATTN 1
 #define SPARROW_OP_DENSE_ATTN 2
 
-/* Shape of one layer's decode batch (host struct, read during the call only). */
+/* Shape of one layer's decode batch (host struct, read during the call only).
+   `landmark` selects the page metadata (SPARROW_LANDMARK_*; 0 = min/max), used by the
+   metadata, append and scoring entry points and ignored by attention. */
 typedef struct sparrow_shape {
     int32_t batch;
     int32_t num_q_heads;
@@ -92,6 +102,7 @@ typedef struct sparrow_shape {
     int32_t page_size;
     int32_t max_pages_per_seq;
     int64_t num_phys_pages;
+    int32_t landmark;
 } sparrow_shape_t;
 
 /*
@@ -107,6 +118,11 @@ typedef struct sparrow_shape {
  * k == n every page is kept (Appendix F: attention is dense while the context
  * fits the budget).  Requires bin_tokens >= 1, n_bins >= 1, frac_den >= 1 and
  * non-negative table entries.
+ *
+ * sink_pages s and local_pages l (0 = pure top-k) force the logical pages
+ * [0, s) (attention sinks) and [n - l, n) (the most recent pages) into the
+ * selection ahead of every scored page, lower index first; the rest of the budget
+ * k goes by score.  Both >= 0.
  */
 typedef struct sparrow_schedule {
     int32_t bin_tokens;
@@ -114,6 +130,8 @@ typedef struct sparrow_schedule {
     const int32_t *min_pages;
     const int32_t *frac_num;
     int32_t frac_den;
+    int32_t sink_pages;
+    int32_t local_pages;
 } sparrow_schedule_t;
 
 /*
@@ -124,6 +142,8 @@ typedef struct sparrow_schedule {
  * [first_pos[b], seq_lens[b]), and for every KV head h and channel i:
  *     meta[phys][h][0][i] = min over the valid tokens t of the page of K[t][i]
  *     meta[phys][h][1][i] = max over the same tokens
+ * (SPARROW_LANDMARK_MEAN: meta[phys][h][i] = the fp32 sum of K[t][i] over the same
+ * tokens, added in token order)
  * where phys = block_table[b][p] and the valid tokens of page p are
  * p*page_size .. min((p+1)*page_size, seq_lens[b]) - 1.  Values are copied
  * exactly (bf16 in, bf16 out); -0 orders below +0.  first_pos == NULL rebuilds
@@ -149,7 +169,7 @@ int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
  *     k_cache[phys][h][slot][:] = k_new[b][h][:],  v_cache[phys][h][slot][:] = v_new[b][h][:]
  * with phys = block_table[b][(L - 1) / page_size], and the page's metadata becomes the
  * channel-wise min/max of its old metadata and the new key (the key itself when the
- * slot is 0).  This equals the metadata rebuilt from the page's L - page*page_size valid
+ * slot is 0); with SPARROW_LANDMARK_MEAN its key sum plus the new key.  This equals the metadata rebuilt from the page's L - page*page_size valid
  * tokens (sparrow_page_meta_update) provided the old metadata described the tokens
  * before L - 1.  Sequences with seq_lens[b] < 1 or seq_lens[b] > max_pages_per_seq *
  * page_size are left untouched.  Sequences must use distinct physical pages.
@@ -172,7 +192,8 @@ int sparrow_append_kv(const sparrow_shape_t *shape, const void *k_new, const voi
  *     S_h(p) = sum over the G query heads j of head h of
  *              sum_i max(q[b][j][i] * mn_i(p), q[b][j][i] * mx_i(p))
  * (an upper bound of q_j . k_t over the tokens of the page), with fp32
- * arithmetic.  k_b is the schedule's budget (see sparrow_schedule_t), capped
+ * arithmetic; with SPARROW_LANDMARK_MEAN, S_h(p) = sum_j q_j . (sum(p) / n_valid(p)),
+ * the query group against the page's mean key.  k_b is the schedule's budget (see sparrow_schedule_t), capped
  * at k_max.  The k_b pages of largest S_h are kept, ties going to the lower
  * page index (-0 equals +0), and written in ascending page order to
  * out_idx[b][h][0 .. k_b); the rest of the row up to k_max is set to -1.
@@ -184,8 +205,8 @@ int sparrow_append_kv(const sparrow_shape_t *shape, const void *k_new, const voi
  * out_idx (device [batch][num_kv_heads][k_max]); workspace of at least
  * sparrow_workspace_size(shape, k_max, SPARROW_OP_SCORE_TOPK) bytes (device,
  * contents need not be initialised); stream.
- * Errors: SPARROW_EINVAL (null pointers, k_max < 1, bad schedule sizes),
- * SPARROW_EUNSUPPORTED, SPARROW_EWORKSPACE, SPARROW_EHIP.
+ * Errors: SPARROW_EINVAL (null pointers, k_max < 1, bad schedule sizes or negative
+ * forced-page counts), SPARROW_EUNSUPPORTED, SPARROW_EWORKSPACE, SPARROW_EHIP.
  */
 int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const void *meta,
                             const int32_t *block_table, const int32_t *seq_lens,

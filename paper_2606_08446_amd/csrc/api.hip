@@ -25,6 +25,8 @@ int check_shape(const sparrow_shape_t *s)
         return SPARROW_EUNSUPPORTED;
     if (s->max_pages_per_seq > SPARROW_MAX_PAGES_PER_SEQ)
         return SPARROW_EUNSUPPORTED;
+    if (s->landmark != SPARROW_LANDMARK_MINMAX && s->landmark != SPARROW_LANDMARK_MEAN)
+        return SPARROW_EUNSUPPORTED;
     if ((int64_t)s->batch * s->num_q_heads > 0x7fffffff / kHeadDim)
         return SPARROW_EINVAL;
     return SPARROW_OK;
@@ -93,7 +95,8 @@ static int score_topk_call(const sparrow_shape_t *shape, const void *q, void *me
         !al4(out_idx) || !al16(workspace))
         return SPARROW_EINVAL;
     if (k_max < 1 || schedule->bin_tokens < 1 || schedule->n_bins < 1 || schedule->frac_den < 1 ||
-        !schedule->min_pages || !schedule->frac_num)
+        !schedule->min_pages || !schedule->frac_num || schedule->sink_pages < 0 ||
+        schedule->local_pages < 0)
         return SPARROW_EINVAL;
     if (shape->batch == 0)
         return SPARROW_OK;
@@ -103,8 +106,9 @@ static int score_topk_call(const sparrow_shape_t *shape, const void *q, void *me
         return SPARROW_EUNSUPPORTED;
     if (!workspace || ws_bytes < score_topk_workspace(*shape))
         return SPARROW_EWORKSPACE;
-    Sched sched{schedule->bin_tokens, schedule->n_bins, schedule->frac_den, schedule->min_pages,
-                schedule->frac_num};
+    Sched sched{schedule->bin_tokens, schedule->n_bins,     schedule->frac_den,
+                schedule->min_pages,  schedule->frac_num, schedule->sink_pages,
+                schedule->local_pages};
     return status_of(launch_score_topk(*shape, q, meta, block_table, seq_lens, sched, k_max,
                                        out_k, out_idx, workspace, app,
                                        static_cast<hipStream_t>(stream)));

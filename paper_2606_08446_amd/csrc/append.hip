@@ -7,6 +7,9 @@
 // row (256 B) and lanes 16-31 the value row.  The page's metadata becomes
 // min/max(old, key) - or the key itself on the page's first slot - which equals the
 // rebuild from all of the page's tokens whenever the old metadata described them.
+// With the mean landmark lane i owns the fp32 sums of channels 4i .. 4i+3 and adds the
+// key's channels to them (the key itself on the page's first slot) - the same fp32 adds,
+// in the same token order, as the rebuild.
 #include "common.h"
 
 namespace sparrow {
@@ -15,11 +18,12 @@ namespace {
 constexpr int kAppendThreads = 256;
 constexpr int kAppendHeads = kAppendThreads / 32;  // KV heads per workgroup
 
+template <bool kMean>
 __global__ __launch_bounds__(kAppendThreads) void k_append_kv(
     const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
     uint16_t *__restrict__ k_cache, uint16_t *__restrict__ v_cache,
     const int32_t *__restrict__ block_table, const int32_t *__restrict__ seq_lens,
-    uint16_t *__restrict__ meta, int num_kv_heads, int ps, int max_pages)
+    void *__restrict__ meta, int num_kv_heads, int ps, int max_pages)
 {
     const int b = blockIdx.x;
     const int h = blockIdx.y * kAppendHeads + (threadIdx.x >> 5);
@@ -41,8 +45,15 @@ __global__ __launch_bounds__(kAppendThreads) void k_append_kv(
         st16(k_cache + crow, kn);
     else
         st16(v_cache + crow, ld16(v_new + nrow));
-    uint16_t *mrow = meta + (phys * num_kv_heads + h) * 2 * kHeadDim + e0;
-    st16(mrow, meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim, tok == 0));
+    if (kMean) {
+        const int c0 = 4 * (threadIdx.x & 31);
+        float *srow = static_cast<float *>(meta) + (phys * num_kv_heads + h) * kHeadDim + c0;
+        const u32x2_t k4 = *reinterpret_cast<const u32x2_t *>(k_new + nrow - i0 + c0);
+        st16(srow, sums_with_key(tok == 0, ld16(srow), k4));
+    } else {
+        uint16_t *mrow = static_cast<uint16_t *>(meta) + (phys * num_kv_heads + h) * 2 * kHeadDim + e0;
+        st16(mrow, meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim, tok == 0));
+    }
 }
 
 }  // namespace
@@ -52,11 +63,18 @@ hipError_t launch_append_kv(const sparrow_shape_t &s, const void *k_new, const v
                             const int32_t *seq_lens, void *meta, hipStream_t stream)
 {
     const dim3 grid(s.batch, (s.num_kv_heads + kAppendHeads - 1) / kAppendHeads);
-    hipLaunchKernelGGL(k_append_kv, grid, dim3(kAppendThreads), 0, stream,
-                       static_cast<const uint16_t *>(k_new), static_cast<const uint16_t *>(v_new),
-                       static_cast<uint16_t *>(k_cache), static_cast<uint16_t *>(v_cache),
-                       block_table, seq_lens, static_cast<uint16_t *>(meta), s.num_kv_heads,
-                       s.page_size, s.max_pages_per_seq);
+    if (s.landmark == SPARROW_LANDMARK_MEAN)
+        hipLaunchKernelGGL(k_append_kv<true>, grid, dim3(kAppendThreads), 0, stream,
+                           static_cast<const uint16_t *>(k_new),
+                           static_cast<const uint16_t *>(v_new), static_cast<uint16_t *>(k_cache),
+                           static_cast<uint16_t *>(v_cache), block_table, seq_lens, meta,
+                           s.num_kv_heads, s.page_size, s.max_pages_per_seq);
+    else
+        hipLaunchKernelGGL(k_append_kv<false>, grid, dim3(kAppendThreads), 0, stream,
+                           static_cast<const uint16_t *>(k_new),
+                           static_cast<const uint16_t *>(v_new), static_cast<uint16_t *>(k_cache),
+                           static_cast<uint16_t *>(v_cache), block_table, seq_lens, meta,
+                           s.num_kv_heads, s.page_size, s.max_pages_per_seq);
     return hipGetLastError();
 }
 

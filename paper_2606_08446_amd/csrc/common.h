@@ -27,6 +27,8 @@ struct Sched {
     int32_t frac_den;
     const int32_t *min_pages;
     const int32_t *frac_num;
+    int32_t sink_pages;   // logical pages [0, sink) always kept
+    int32_t local_pages;  // logical pages [n - local, n) always kept
 };
 
 __device__ __forceinline__ u32x4_t ld16(const void *p)
@@ -94,6 +96,18 @@ __device__ __forceinline__ u32x4_t meta_with_key(u32x4_t old, u32x4_t key, bool 
         }
         r[w] = out;
     }
+    return r;
+}
+
+// Mean landmark: fp32 key sums of 4 channels after one more key (4 bf16 in `k4`); a fresh
+// page (its first token) takes the key itself (the rebuild's 0 + k).
+__device__ __forceinline__ u32x4_t sums_with_key(bool fresh, u32x4_t old, u32x2_t k4)
+{
+    const float k[4] = {bf16_lo(k4[0]), bf16_hi(k4[0]), bf16_lo(k4[1]), bf16_hi(k4[1])};
+    u32x4_t r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        r[e] = __float_as_uint(fresh ? 0.f + k[e] : __uint_as_float(old[e]) + k[e]);
     return r;
 }
 

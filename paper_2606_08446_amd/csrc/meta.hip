@@ -8,6 +8,9 @@
 // min/max in registers and writes two 16-byte rows.  Min/max run on an integer image of
 // the bf16 bit pattern whose order is the total order of the values (-0 below +0), so
 // the result is one of the input patterns, bit for bit.
+//
+// With the mean landmark the thread instead sums its 8 channels over the page's tokens in
+// token order (fp32 adds of exactly converted bf16 keys) and writes 8 fp32 sums.
 #include "common.h"
 
 namespace sparrow {
@@ -63,11 +66,43 @@ __device__ __forceinline__ void slice_minmax(const uint16_t *__restrict__ src, i
     st16(dst + kHeadDim, hi);
 }
 
+// Key sums of one (page, head, 8-channel slice) over `valid` tokens, in token order.
 template <int PS>
+__device__ __forceinline__ void slice_sum(const uint16_t *__restrict__ src, int valid,
+                                          float *__restrict__ dst)
+{
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        acc[e] = 0.f;
+    for (int t0 = 0; t0 < PS; t0 += 16) {
+        if (t0 >= valid)
+            break;
+        const int nt = valid - t0 < 16 ? valid - t0 : 16;
+        u32x4_t v[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t)
+            v[t] = (t < nt) ? ld16(src + (size_t)(t0 + t) * kHeadDim) : (u32x4_t){0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            if (t < nt) {
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    acc[2 * w] += bf16_lo(v[t][w]);
+                    acc[2 * w + 1] += bf16_hi(v[t][w]);
+                }
+            }
+        }
+    }
+    st16(dst, __builtin_bit_cast(u32x4_t, (f32x4_t){acc[0], acc[1], acc[2], acc[3]}));
+    st16(dst + 4, __builtin_bit_cast(u32x4_t, (f32x4_t){acc[4], acc[5], acc[6], acc[7]}));
+}
+
+template <int PS, bool kMean>
 __global__ __launch_bounds__(kMetaThreads) void k_meta_update(
     const uint16_t *__restrict__ k_cache, const int32_t *__restrict__ block_table,
     const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ first_pos,
-    uint16_t *__restrict__ meta, int num_kv_heads, int max_pages, int rebuild)
+    void *__restrict__ meta, int num_kv_heads, int max_pages, int rebuild)
 {
     const int b = rebuild ? blockIdx.y : blockIdx.x;
     const int L = clamp_len(seq_lens[b], PS, max_pages);
@@ -92,8 +127,14 @@ __global__ __launch_bounds__(kMetaThreads) void k_meta_update(
             const int h = u >> 4;
             const int c = u & 15;
             const uint16_t *src = k_cache + ((phys * num_kv_heads + h) * PS) * kHeadDim + c * 8;
-            uint16_t *dst = meta + ((phys * num_kv_heads + h) * 2) * kHeadDim + c * 8;
-            slice_minmax<PS>(src, valid, dst);
+            if (kMean) {
+                float *dst = static_cast<float *>(meta) + (phys * num_kv_heads + h) * kHeadDim + c * 8;
+                slice_sum<PS>(src, valid, dst);
+            } else {
+                uint16_t *dst = static_cast<uint16_t *>(meta) +
+                                ((phys * num_kv_heads + h) * 2) * kHeadDim + c * 8;
+                slice_minmax<PS>(src, valid, dst);
+            }
         }
     }
 }
@@ -104,10 +145,14 @@ hipError_t launch_ps(const sparrow_shape_t &s, const void *k_cache, const int32_
 {
     const int rebuild = first_pos == nullptr;
     const dim3 grid = rebuild ? dim3(s.max_pages_per_seq, s.batch) : dim3(s.batch);
-    hipLaunchKernelGGL(k_meta_update<PS>, grid, dim3(kMetaThreads), 0, st,
-                       static_cast<const uint16_t *>(k_cache), bt, lens, first_pos,
-                       static_cast<uint16_t *>(meta), s.num_kv_heads, s.max_pages_per_seq,
-                       rebuild);
+    if (s.landmark == SPARROW_LANDMARK_MEAN)
+        hipLaunchKernelGGL((k_meta_update<PS, true>), grid, dim3(kMetaThreads), 0, st,
+                           static_cast<const uint16_t *>(k_cache), bt, lens, first_pos, meta,
+                           s.num_kv_heads, s.max_pages_per_seq, rebuild);
+    else
+        hipLaunchKernelGGL((k_meta_update<PS, false>), grid, dim3(kMetaThreads), 0, st,
+                           static_cast<const uint16_t *>(k_cache), bt, lens, first_pos, meta,
+                           s.num_kv_heads, s.max_pages_per_seq, rebuild);
     return hipGetLastError();
 }
 

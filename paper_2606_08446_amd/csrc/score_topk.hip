@@ -71,6 +71,23 @@ __device__ __forceinline__ float lane_dot(const float (&w)[8], u32x4_t v)
     return acc;
 }
 
+// Mean landmark: 4 fp32 key sums against the lane's 4 weights, in a fixed FMA order.
+__device__ __forceinline__ float lane_dot4(const float (&w)[8], u32x4_t v)
+{
+    float acc = 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+        acc = fmaf(w[t], __uint_as_float(v[t]), acc);
+    return acc;
+}
+
+// Valid tokens of logical page p of a sequence of L tokens.
+__device__ __forceinline__ int page_tokens(int p, int L, int ps)
+{
+    const int left = L - p * ps;
+    return left < ps ? left : ps;
+}
+
 // One workgroup scores kScorePages consecutive logical pages of one sequence for up to
 // kScoreHeads KV heads.  A wave owns a pair of KV heads: each load instruction reads the
 // two heads' metadata rows of one page, 1 KiB contiguous (lanes 0-31 the first head,
@@ -83,7 +100,7 @@ __device__ __forceinline__ float lane_dot(const float (&w)[8], u32x4_t v)
 // wave that scores a sequence's last page writes the new key/value rows of its two heads
 // and the page's updated metadata (lane slices of [mn | mx] are exactly the slices
 // meta_with_key works on), and scores that page from the updated slice it holds.
-template <bool kAppend>
+template <bool kAppend, bool kMean>
 __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ meta,
     const int32_t *__restrict__ block_table, const int32_t *__restrict__ seq_lens, Sched sched,
@@ -122,12 +139,24 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const bool active = sub < wpp;
     const bool lane_on = active && head < nh;
 
-    // Weights: 8 consecutive elements of Q- (mn half) or Q+ (mx half) of this lane's head.
+    // Weights: 8 consecutive elements of Q- (mn half) or Q+ (mx half) of this lane's head;
+    // with the mean landmark, channels 4 li .. 4 li + 3 of the group's summed queries (the
+    // lane's 16 bytes of the row are 4 fp32 key sums).
     float w[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j)
         w[j] = 0.f;
-    if (lane_on) {
+    if (kMean && lane_on) {
+        const uint16_t *qh =
+            q + ((int64_t)b * num_q_heads + (int64_t)(h0 + head) * G) * kHeadDim + 4 * li;
+        for (int g = 0; g < G; ++g) {
+            const u32x2_t v = *reinterpret_cast<const u32x2_t *>(qh + g * kHeadDim);
+            w[0] += bf16_lo(v[0]);
+            w[1] += bf16_hi(v[0]);
+            w[2] += bf16_lo(v[1]);
+            w[3] += bf16_hi(v[1]);
+        }
+    } else if (lane_on) {
         const int i0 = e0 & (kHeadDim - 1);
         const bool neg = e0 < kHeadDim;
         const uint16_t *qh = q + ((int64_t)b * num_q_heads + (int64_t)(h0 + head) * G) * kHeadDim + i0;
@@ -162,7 +191,13 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
             // The metadata row of this page is read and written only here.
             uint16_t *mrow = const_cast<uint16_t *>(meta) +
                              (phys * num_kv_heads + hh) * 2 * kHeadDim + e0;
-            upd = meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim, tok == 0);
+            if (kMean) {
+                const u32x2_t k4 = *reinterpret_cast<const u32x2_t *>(
+                    static_cast<const uint16_t *>(app.k_new) + nrow - i0 + 4 * li);
+                upd = sums_with_key(tok == 0, tok == 0 ? upd : ld16(mrow), k4);
+            } else {
+                upd = meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim, tok == 0);
+            }
             st16(mrow, upd);
             last_slot = slot;
         }
@@ -204,26 +239,28 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
         float part[kScoreBatch];
 #pragma unroll
         for (int j = 0; j < kScoreBatch; ++j)
-            part[j] = lane_dot(w, cur[j]);
+            part[j] = kMean ? lane_dot4(w, cur[j]) : lane_dot(w, cur[j]);
         const float total = butterfly8(part, li);
         const int j = j0 + (li & 7);
+        const int slot = sub + wpp * j;
         // (the appended page was read here before its update landed: its score is
         // written below instead)
         if (li < kScoreBatch && j < my_pages && head < nh &&
-            !(kAppend && sub + wpp * j == last_slot))
-            out[sub + wpp * j] = total;
+            !(kAppend && slot == last_slot))
+            out[slot] = kMean ? total / (float)page_tokens(page0 + slot, L, ps) : total;
     }
     if (kAppend && last_slot >= 0) {
         // Score of the appended page from the updated slice: the same per-lane FMA chain,
         // and a 32-lane xor reduction (1, 2, 4, 8, 16) - the same tree of additions that
         // butterfly8 applies to every page, so the score is bit-identical to scoring the
         // updated metadata from memory.
-        float total = lane_dot(w, upd);
+        float total = kMean ? lane_dot4(w, upd) : lane_dot(w, upd);
 #pragma unroll
         for (int x = 1; x < 32; x <<= 1)
             total += __shfl_xor(total, x, 64);
         if (li == 0)
-            out[last_slot] = total;
+            out[last_slot] =
+                kMean ? total / (float)page_tokens(page0 + last_slot, L, ps) : total;
     }
 }
 
@@ -298,7 +335,9 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         for (int j = 0; j < kTopkBatch; ++j) {
             const int i = base + tid + kTopkThreads * j;
             if (i < n) {
-                const uint32_t key = score_key(v[j]);
+                // forced pages (sinks, most recent pages) outrank every score
+                const bool forced = i < sched.sink_pages || i >= n - sched.local_pages;
+                const uint32_t key = forced ? 0xffffffffu : score_key(v[j]);
                 keys[i] = key;
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
@@ -459,16 +498,14 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta
     const int units = s.batch * s.num_kv_heads;
     const dim3 sgrid((s.max_pages_per_seq + kScorePages - 1) / kScorePages, s.batch,
                      (s.num_kv_heads + kScoreHeads - 1) / kScoreHeads);
-    if (app.k_new != nullptr)
-        hipLaunchKernelGGL(k_page_score<true>, sgrid, dim3(kScoreThreads), 0, stream,
-                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
-                           block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
-                           s.page_size, s.max_pages_per_seq, scores, app);
-    else
-        hipLaunchKernelGGL(k_page_score<false>, sgrid, dim3(kScoreThreads), 0, stream,
-                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
-                           block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
-                           s.page_size, s.max_pages_per_seq, scores, app);
+    const bool mean = s.landmark == SPARROW_LANDMARK_MEAN;
+    const bool append = app.k_new != nullptr;
+    auto kernel = append ? (mean ? k_page_score<true, true> : k_page_score<true, false>)
+                         : (mean ? k_page_score<false, true> : k_page_score<false, false>);
+    hipLaunchKernelGGL(kernel, sgrid, dim3(kScoreThreads), 0, stream,
+                       static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
+                       block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
+                       s.page_size, s.max_pages_per_seq, scores, app);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;

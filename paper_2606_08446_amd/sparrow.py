@@ -30,6 +30,8 @@ SPARROW_MAX_PAGES_PER_SEQ = 15360
 SPARROW_MAX_BATCH = 8192
 SPARROW_OUT_F32 = 0
 SPARROW_OUT_BF16 = 1
+SPARROW_LANDMARK_MINMAX = 0
+SPARROW_LANDMARK_MEAN = 1
 SPARROW_LOGITS_F32 = 0
 SPARROW_LOGITS_BF16 = 1
 SPARROW_OP_SCORE_TOPK = 0
@@ -52,13 +54,14 @@ class Shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
-                ("num_phys_pages", ctypes.c_int64)]
+                ("num_phys_pages", ctypes.c_int64), ("landmark", ctypes.c_int32)]
 
 
 class Schedule(ctypes.Structure):
     _fields_ = [("bin_tokens", ctypes.c_int32), ("n_bins", ctypes.c_int32),
                 ("min_pages", ctypes.c_void_p), ("frac_num", ctypes.c_void_p),
-                ("frac_den", ctypes.c_int32)]
+                ("frac_den", ctypes.c_int32), ("sink_pages", ctypes.c_int32),
+                ("local_pages", ctypes.c_int32)]
 
 
 _lib = None
@@ -172,16 +175,26 @@ status_string = sparrow_status_string
 
 # ------------------------------------------------------------------ host helpers
 def make_shape(batch, num_q_heads, num_kv_heads, page_size, max_pages_per_seq, num_phys_pages,
-               head_dim=128) -> Shape:
+               head_dim=128, landmark=SPARROW_LANDMARK_MINMAX) -> Shape:
     return Shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq,
-                 num_phys_pages)
+                 num_phys_pages, landmark)
 
 
-def shape_of(q, k_cache, block_table) -> Shape:
+def shape_of(q, k_cache, block_table, landmark=SPARROW_LANDMARK_MINMAX) -> Shape:
     """Shape struct from tensors q [B][Hq][D], k_cache [P][Hkv][ps][D], block_table [B][M]."""
     B, Hq, D = q.shape
     P, Hkv, ps, _ = k_cache.shape
-    return make_shape(B, Hq, Hkv, ps, block_table.shape[1], P, head_dim=D)
+    return make_shape(B, Hq, Hkv, ps, block_table.shape[1], P, head_dim=D, landmark=landmark)
+
+
+def new_meta(num_phys_pages, num_kv_heads, device, landmark=SPARROW_LANDMARK_MINMAX):
+    """A zeroed metadata buffer of the given landmark: bf16 [P][Hkv][2][128] (min/max) or fp32
+    [P][Hkv][128] (key sums) - 512 bytes per (page, head) either way."""
+    import torch
+    if landmark == SPARROW_LANDMARK_MEAN:
+        return torch.zeros((num_phys_pages, num_kv_heads, 128), dtype=torch.float32, device=device)
+    return torch.zeros((num_phys_pages, num_kv_heads, 2, 128), dtype=torch.bfloat16,
+                       device=device)
 
 
 def budget_bound(seq_lens: Sequence[int], page_size: int, bin_tokens: int,
@@ -225,38 +238,44 @@ def _require_device(t):
 
 
 # ------------------------------------------------------------------ tensor-level wrappers
-def page_meta_update(k_cache, block_table, seq_lens, meta, first_pos=None, shape=None):
-    """Rebuild (first_pos None) or update the min/max metadata in ``meta`` (in place)."""
+def page_meta_update(k_cache, block_table, seq_lens, meta, first_pos=None, shape=None,
+                     landmark=SPARROW_LANDMARK_MINMAX):
+    """Rebuild (first_pos None) or update the page metadata in ``meta`` (in place)."""
     _require_device(k_cache)
     if shape is None:
         P, Hkv, ps, D = k_cache.shape
-        shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D)
+        shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D,
+                           landmark=landmark)
     rc = sparrow_page_meta_update(shape, _ptr(k_cache), _ptr(block_table), _ptr(seq_lens),
                                   _ptr(first_pos), _ptr(meta), _stream(k_cache.device))
     _check("sparrow_page_meta_update", rc)
     return meta
 
 
-def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta):
+def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta,
+              landmark=SPARROW_LANDMARK_MINMAX):
     """Write token ``seq_lens[b] - 1`` of every sequence into the caches and update the
     metadata of its page (all in place)."""
     _require_device(k_cache)
     P, Hkv, ps, D = k_cache.shape
-    shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D)
+    shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D,
+                       landmark=landmark)
     rc = sparrow_append_kv(shape, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
                            _ptr(block_table), _ptr(seq_lens), _ptr(meta), _stream(k_cache.device))
     _check("sparrow_append_kv", rc)
 
 
 def page_score_topk(q, meta, block_table, seq_lens, k_cache_shape, min_pages, frac_num,
-                    frac_den, bin_tokens, k_max, out_k=None, out_idx=None, workspace=None):
+                    frac_den, bin_tokens, k_max, out_k=None, out_idx=None, workspace=None,
+                    landmark=SPARROW_LANDMARK_MINMAX, sink_pages=0, local_pages=0):
     """Scores, budgets and top-k page lists.  Returns (k [B] int32, idx [B][Hkv][k_max] int32)."""
     import torch
     _require_device(q)
     P, Hkv, ps, D = k_cache_shape
-    shape = make_shape(q.shape[0], q.shape[1], Hkv, ps, block_table.shape[1], P, D)
+    shape = make_shape(q.shape[0], q.shape[1], Hkv, ps, block_table.shape[1], P, D,
+                       landmark=landmark)
     sched = Schedule(int(bin_tokens), int(min_pages.numel()), _ptr(min_pages), _ptr(frac_num),
-                     int(frac_den))
+                     int(frac_den), int(sink_pages), int(local_pages))
     dev = q.device
     if out_k is None:
         out_k = torch.empty(q.shape[0], dtype=torch.int32, device=dev)
@@ -369,14 +388,15 @@ class SparseDecodeStep:
     ``first_pos`` (skipped when None), page scoring + top-k, sparse attention."""
 
     def __init__(self, q, k_cache, v_cache, block_table, seq_lens, meta, min_pages, frac_num,
-                 frac_den, bin_tokens, k_max, scale=None):
+                 frac_den, bin_tokens, k_max, scale=None, landmark=SPARROW_LANDMARK_MINMAX,
+                 sink_pages=0, local_pages=0):
         import torch
         _require_device(q)
         self.q, self.k_cache, self.v_cache = q, k_cache, v_cache
         self.block_table, self.seq_lens, self.meta = block_table, seq_lens, meta
-        self.shape = shape_of(q, k_cache, block_table)
+        self.shape = shape_of(q, k_cache, block_table, landmark=landmark)
         self.sched = Schedule(int(bin_tokens), int(min_pages.numel()), _ptr(min_pages),
-                              _ptr(frac_num), int(frac_den))
+                              _ptr(frac_num), int(frac_den), int(sink_pages), int(local_pages))
         self._tables = (min_pages, frac_num)
         self.k_max = int(k_max)
         self.scale = 1.0 / math.sqrt(q.shape[2]) if scale is None else float(scale)

@@ -37,6 +37,14 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, name), name
 
 
+def test_struct_layouts_match_the_header():
+    # the binding's structs must have the header's field order and sizes
+    import ctypes
+    assert ctypes.sizeof(S.Shape) == 40 and S.Shape.landmark.offset == 32
+    assert S.Schedule.sink_pages.offset == 28 and S.Schedule.local_pages.offset == 32
+    assert ctypes.sizeof(S.Schedule) == 40
+
+
 def test_header_constants_match_binding():
     text = open(HEADER).read()
     consts = dict(re.findall(r"#define (SPARROW_\w+) \(?(-?\d+)\)?", text))
@@ -62,6 +70,8 @@ BAD_SHAPES = [
     (dict(batch=-1), S.SPARROW_EINVAL),
     (dict(num_kv_heads=0), S.SPARROW_EINVAL),
     (dict(num_phys_pages=0), S.SPARROW_EINVAL),
+    (dict(landmark=2), S.SPARROW_EUNSUPPORTED),
+    (dict(landmark=-1), S.SPARROW_EUNSUPPORTED),
 ]
 
 
@@ -141,6 +151,10 @@ def test_null_shape_and_schedule_are_rejected(lib):
     assert call("topk", good_shape(), sched=S.Schedule(2048, 1, FAKE, FAKE, 0)) == S.SPARROW_EINVAL
     assert call("topk", good_shape(), sched=S.Schedule(2048, 1, None, FAKE, 10)) == S.SPARROW_EINVAL
     assert call("topk", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), sched=S.Schedule(2048, 1, FAKE, FAKE, 10, -1, 0)) == \
+        S.SPARROW_EINVAL
+    assert call("fused", good_shape(), sched=S.Schedule(2048, 1, FAKE, FAKE, 10, 0, -3)) == \
+        S.SPARROW_EINVAL
     assert call("fused", good_shape(), k_max=0) == S.SPARROW_EINVAL
     assert call("fused", good_shape(), sched=S.Schedule(2048, 1, FAKE, None, 10)) == \
         S.SPARROW_EINVAL
