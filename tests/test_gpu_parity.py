@@ -186,7 +186,7 @@ def test_meta_update_larger_pages(ps):
 def test_full_budget_sparse_equals_dense_bitwise():
     log("case full budget == dense")
     inp = small_inputs(4, 2, 16, (3000, 777, 16), seed=16, schedule=W.fixed_budget(10000))
-    k_max = inp.max_pages  # same split plan as the dense call
+    k_max = inp.max_pages  # every page listed: the same wave partition as the dense call
     g = gpu_run(inp, k_max)
     np.testing.assert_array_equal(g["out_sparse"], g["out_dense"])
 
