@@ -346,3 +346,29 @@ def test_workspace_reuse_across_sizes():
         if trial == 0:
             ref_d = oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], SCALE)
         check_out(dense.cpu().numpy().astype(np.float64), ref_d, f"reuse dense {trial}")
+
+
+# ---------------------------------------------------------------------------------- limits
+def test_longest_sequence_the_block_table_allows():
+    # SPARROW_MAX_PAGES_PER_SEQ pages of 16 tokens (245760 tokens) in one sequence, next to a
+    # short one: the top-k keeps 15360 keys in LDS, the attention plan spans both.
+    log("case max pages per sequence")
+    n_max = S.SPARROW_MAX_PAGES_PER_SEQ
+    lengths = (16 * n_max, 5000)
+    w = W.small(B=2, Hq=8, Hkv=1, ps=16, lengths=lengths, seed=31,
+                schedule=W.fraction_budget(1, 20, floor_pages=4), extra_pages=0)
+    inp = W.generate(w, DEV, lengths=list(lengths))
+    assert inp.max_pages == n_max
+    full_check(inp)
+
+
+def test_largest_batch():
+    # SPARROW_MAX_BATCH ragged sequences (many empty or shorter than a page).
+    log("case max batch")
+    B = S.SPARROW_MAX_BATCH
+    rng = np.random.default_rng(32)
+    lengths = tuple(int(x) for x in rng.integers(0, 70, size=B))
+    w = W.small(B=B, Hq=2, Hkv=1, ps=16, lengths=lengths, seed=32,
+                schedule=W.fraction_budget(1, 2, floor_pages=1))
+    inp = W.generate(w, DEV, lengths=list(lengths))
+    full_check(inp)
