@@ -3,9 +3,12 @@
 //
 // k_acceptance: alpha_t = sum_x min(p(x), q(x)) with p, q the softmax of the target and draft
 // logit rows at inverse temperature tau.  One 1024-thread workgroup per token makes two
-// passes over its two rows: an online log-sum-exp of both (plain loads, so the rows stay in
-// the Infinity Cache for the second pass), then sum_x exp(min(tau a_x - P, tau b_x - Q)) -
-// one exp per vocabulary entry, since min(e^u, e^v) = e^min(u, v) - with non-temporal loads.
+// passes over its two rows: an online log-sum-exp of both (plain loads), then
+// sum_x exp(min(tau a_x - P, tau b_x - Q)) - one exp per vocabulary entry, since
+// min(e^u, e^v) = e^min(u, v) - with non-temporal loads, from the end of the rows back, so
+// the part read last in the first pass is read first again while the L2 may still hold
+// it.  The launch reserves LDS for one workgroup per CU, which keeps the rows in flight
+// (and so the traffic between the two reads of an element) small.
 // Rows are read as 16-byte vectors; a row that does not start 16-byte aligned is handled
 // with scalar head and tail elements.  Accumulation is fp32 per thread, tree reductions
 // across the workgroup.
@@ -187,7 +190,7 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
     const float P = a.m + __logf(a.s);
     const float Q = b.m + __logf(b.s);
 
-    // ---- pass 2: sum of exp(min(tau a - P, tau b - Q))
+    // ---- pass 2: sum of exp(min(tau a - P, tau b - Q)), vectors in reverse order
     float acc = 0.f;
     for (int i = tid; i < head; i += kAccThreads)
         acc += __expf(fminf(tau * Logit<T>::at(pr, i) - P, tau * Logit<T>::at(qr, i) - Q));
@@ -198,8 +201,8 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
         u32x4_t ra[4], rb[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            ra[u] = ld16_nt(pv + v + u * kAccThreads);
-            rb[u] = ld16_nt(qv + v + u * kAccThreads);
+            ra[u] = ld16_nt(pv + (nvec - 1 - (v + u * kAccThreads)));
+            rb[u] = ld16_nt(qv + (nvec - 1 - (v + u * kAccThreads)));
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -213,8 +216,8 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
     }
     for (; v < nvec; v += kAccThreads) {
         float xa[W], xb[W];
-        Logit<T>::unpack(pv[v], xa);
-        Logit<T>::unpack(qv[v], xb);
+        Logit<T>::unpack(pv[nvec - 1 - v], xa);
+        Logit<T>::unpack(qv[nvec - 1 - v], xb);
 #pragma unroll
         for (int e = 0; e < W; ++e)
             acc += __expf(fminf(tau * xa[e] - P, tau * xb[e] - Q));
@@ -403,14 +406,16 @@ __global__ __launch_bounds__(kTailThreads) void k_tail_stats(
 hipError_t launch_acceptance(int64_t T, int V, int dtype, const void *target, const void *draft,
                              float tau, float *alpha, hipStream_t stream)
 {
+    // Unused dynamic LDS: with it only one workgroup fits on a CU.
+    constexpr size_t kOnePerCu = 96 * 1024;
     if (dtype == SPARROW_LOGITS_BF16)
-        hipLaunchKernelGGL(k_acceptance<uint16_t>, dim3((unsigned)T), dim3(kAccThreads), 0,
-                           stream, static_cast<const uint16_t *>(target),
+        hipLaunchKernelGGL(k_acceptance<uint16_t>, dim3((unsigned)T), dim3(kAccThreads),
+                           kOnePerCu, stream, static_cast<const uint16_t *>(target),
                            static_cast<const uint16_t *>(draft), V, tau, alpha);
     else
-        hipLaunchKernelGGL(k_acceptance<float>, dim3((unsigned)T), dim3(kAccThreads), 0, stream,
-                           static_cast<const float *>(target), static_cast<const float *>(draft),
-                           V, tau, alpha);
+        hipLaunchKernelGGL(k_acceptance<float>, dim3((unsigned)T), dim3(kAccThreads), kOnePerCu,
+                           stream, static_cast<const float *>(target),
+                           static_cast<const float *>(draft), V, tau, alpha);
     return hipGetLastError();
 }
 
