@@ -57,6 +57,7 @@ CASES = [  # (G, Hkv, ps, lengths)
     (5, 3, 32, (33, 64, 65, 1, 200)),
     (1, 9, 64, (64, 65, 130, 7, 300)),
     (4, 8, 128, (128, 129, 1, 260, 600)),
+    (2, 12, 16, (15, 16, 17, 500)),  # a partial group of 8 heads per scoring workgroup
 ]
 
 

@@ -58,6 +58,11 @@ SWEEP = [
     (4, 2, 64, (64, 65, 9000), W.fraction_budget(1, 5)),
     (2, 2, 128, (127, 128, 129, 30000), W.fraction_budget(1, 6)),
     (3, 2, 16, (0, 50, 0, 1200), W.fraction_budget(1, 2)),
+    # KV-head counts that leave a partial group of 8 heads per scoring workgroup, an odd
+    # head in a wave's head pair, or an idle wave
+    (1, 9, 16, (3000, 17, 900), W.fraction_budget(1, 5)),
+    (2, 12, 32, (5000, 64, 1), W.fraction_budget(1, 4)),
+    (3, 5, 16, (2048, 2049, 333), W.fraction_budget(1, 3)),
 ]
 
 
