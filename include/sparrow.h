@@ -27,9 +27,12 @@
  *    each call only validates its host-visible arguments and enqueues kernels
  *    on `stream` (a hipStream_t passed as void*; NULL = the null stream).
  *  - Return value: SPARROW_OK (0) or a negative status (see below).  Nothing is
- *    enqueued when a negative status is returned.  Faults caused by bad device
- *    contents (for example a block-table entry outside [0, num_phys_pages))
- *    are the caller's contract and surface at the caller's next synchronisation.
+ *    enqueued when a negative status is returned.  Device contents are checked
+ *    only where an index could leave a buffer: a block-table entry outside
+ *    [0, num_phys_pages) marks an absent page - no kernel reads or writes that
+ *    physical page; scoring sees zero metadata for it (score 0), attention
+ *    leaves its tokens out, and an append to it writes nothing - and page
+ *    indices, lengths and budgets are clamped to what the shape allows.
  *  - bf16 tensors are IEEE bfloat16 bit patterns.  NaN inputs are not supported.
  *  - Alignment: q, k_cache, v_cache, meta, out and workspace start on a 16-byte
  *    boundary and the int32 arrays on a 4-byte boundary (any hipMalloc or PyTorch

@@ -23,7 +23,7 @@ __global__ __launch_bounds__(kAppendThreads) void k_append_kv(
     const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
     uint16_t *__restrict__ k_cache, uint16_t *__restrict__ v_cache,
     const int32_t *__restrict__ block_table, const int32_t *__restrict__ seq_lens,
-    void *__restrict__ meta, int num_kv_heads, int ps, int max_pages)
+    void *__restrict__ meta, int num_kv_heads, int ps, int max_pages, int64_t num_phys)
 {
     const int b = blockIdx.x;
     const int h = blockIdx.y * kAppendHeads + (threadIdx.x >> 5);
@@ -38,6 +38,8 @@ __global__ __launch_bounds__(kAppendThreads) void k_append_kv(
     const int e0 = 8 * (threadIdx.x & 31);  // element of [mn | mx]
     const int i0 = e0 & (kHeadDim - 1);     // channel
     const int64_t phys = block_table[(int64_t)b * max_pages + lp];
+    if (phys < 0 || phys >= num_phys)
+        return;  // the page is outside the cache: nothing is written
     const int64_t nrow = ((int64_t)b * num_kv_heads + h) * kHeadDim + i0;
     const u32x4_t kn = ld16(k_new + nrow);
     const int64_t crow = ((phys * num_kv_heads + h) * ps + tok) * kHeadDim + i0;
@@ -68,13 +70,13 @@ hipError_t launch_append_kv(const sparrow_shape_t &s, const void *k_new, const v
                            static_cast<const uint16_t *>(k_new),
                            static_cast<const uint16_t *>(v_new), static_cast<uint16_t *>(k_cache),
                            static_cast<uint16_t *>(v_cache), block_table, seq_lens, meta,
-                           s.num_kv_heads, s.page_size, s.max_pages_per_seq);
+                           s.num_kv_heads, s.page_size, s.max_pages_per_seq, s.num_phys_pages);
     else
         hipLaunchKernelGGL(k_append_kv<false>, grid, dim3(kAppendThreads), 0, stream,
                            static_cast<const uint16_t *>(k_new),
                            static_cast<const uint16_t *>(v_new), static_cast<uint16_t *>(k_cache),
                            static_cast<uint16_t *>(v_cache), block_table, seq_lens, meta,
-                           s.num_kv_heads, s.page_size, s.max_pages_per_seq);
+                           s.num_kv_heads, s.page_size, s.max_pages_per_seq, s.num_phys_pages);
     return hipGetLastError();
 }
 

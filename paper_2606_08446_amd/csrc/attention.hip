@@ -48,6 +48,7 @@ struct AttnArgs {
     float *ml_part;
     void *out;
     int k_max, batch, num_q_heads, num_kv_heads, ps, max_pages, out_bf16, total_waves;
+    int64_t num_phys;  // physical pages in the caches
     float scale_log2;
 };
 
@@ -143,7 +144,7 @@ struct Cursor {
 struct Batch {
     int b, h, j0, n, L;
     bool ends_unit;
-    int phys;  // physical page (-1: entry outside the sequence)
+    int phys;  // physical page (-1: entry outside the sequence or the cache)
     int tok0;  // first token of the page
 };
 
@@ -170,8 +171,10 @@ __device__ __forceinline__ void fetch_batch(const AttnArgs &a, const int32_t *s_
     if (lane < n) {
         const int lp = kSparse ? a.idx[((int64_t)c.b * Hkv + c.h) * a.k_max + c.j + lane]
                                : c.j + lane;
-        if (lp >= 0 && lp < np)
-            t.phys = a.block_table[(int64_t)c.b * a.max_pages + lp];
+        if (lp >= 0 && lp < np) {
+            const int pp = a.block_table[(int64_t)c.b * a.max_pages + lp];
+            t.phys = pp >= 0 && pp < a.num_phys ? pp : -1;  // outside the cache: absent
+        }
         t.tok0 = lp * a.ps;
     }
     c.pos += n;
@@ -554,6 +557,7 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     a.num_kv_heads = s.num_kv_heads;
     a.ps = s.page_size;
     a.max_pages = s.max_pages_per_seq;
+    a.num_phys = s.num_phys_pages;
     a.out_bf16 = out_dtype == SPARROW_OUT_BF16 ? 1 : 0;
     a.total_waves = device_waves();
     a.scale_log2 = scale * 1.4426950408889634f;

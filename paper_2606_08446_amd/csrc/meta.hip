@@ -102,7 +102,7 @@ template <int PS, bool kMean>
 __global__ __launch_bounds__(kMetaThreads) void k_meta_update(
     const uint16_t *__restrict__ k_cache, const int32_t *__restrict__ block_table,
     const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ first_pos,
-    void *__restrict__ meta, int num_kv_heads, int max_pages, int rebuild)
+    void *__restrict__ meta, int num_kv_heads, int max_pages, int64_t num_phys, int rebuild)
 {
     const int b = rebuild ? blockIdx.y : blockIdx.x;
     const int L = clamp_len(seq_lens[b], PS, max_pages);
@@ -122,6 +122,8 @@ __global__ __launch_bounds__(kMetaThreads) void k_meta_update(
     const int slices = num_kv_heads * (kHeadDim / 8);
     for (int p = p_begin; p < p_end; ++p) {
         const int64_t phys = block_table[(int64_t)b * max_pages + p];
+        if (phys < 0 || phys >= num_phys)
+            continue;  // an entry outside the cache: an absent page, nothing to build
         const int valid = L - p * PS < PS ? L - p * PS : PS;
         for (int u = threadIdx.x; u < slices; u += kMetaThreads) {
             const int h = u >> 4;
@@ -148,11 +150,11 @@ hipError_t launch_ps(const sparrow_shape_t &s, const void *k_cache, const int32_
     if (s.landmark == SPARROW_LANDMARK_MEAN)
         hipLaunchKernelGGL((k_meta_update<PS, true>), grid, dim3(kMetaThreads), 0, st,
                            static_cast<const uint16_t *>(k_cache), bt, lens, first_pos, meta,
-                           s.num_kv_heads, s.max_pages_per_seq, rebuild);
+                           s.num_kv_heads, s.max_pages_per_seq, s.num_phys_pages, rebuild);
     else
         hipLaunchKernelGGL((k_meta_update<PS, false>), grid, dim3(kMetaThreads), 0, st,
                            static_cast<const uint16_t *>(k_cache), bt, lens, first_pos, meta,
-                           s.num_kv_heads, s.max_pages_per_seq, rebuild);
+                           s.num_kv_heads, s.max_pages_per_seq, s.num_phys_pages, rebuild);
     return hipGetLastError();
 }
 

@@ -104,7 +104,7 @@ template <bool kAppend, bool kMean>
 __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ meta,
     const int32_t *__restrict__ block_table, const int32_t *__restrict__ seq_lens, Sched sched,
-    int k_max, int num_q_heads, int num_kv_heads, int ps, int max_pages,
+    int k_max, int num_q_heads, int num_kv_heads, int ps, int max_pages, int64_t num_phys,
     float *__restrict__ scores, AppendArgs app)
 {
     __shared__ int32_t s_phys[kScorePages];
@@ -127,8 +127,10 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const int li = lane & 31;
     const int e0 = 8 * li;  // first element of this lane in the [mn | mx] row
 
-    if (tid < npg)
-        s_phys[tid] = block_table[(int64_t)b * max_pages + page0 + tid];
+    if (tid < npg) {  // -1: an entry outside the cache, an absent page (score 0)
+        const int pp = block_table[(int64_t)b * max_pages + page0 + tid];
+        s_phys[tid] = pp >= 0 && pp < num_phys ? pp : -1;
+    }
 
     // Wave -> (head pair, page subset).
     const int npairs = (nh + 1) >> 1;
@@ -180,26 +182,29 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
             const int tok = L - 1 - (n - 1) * ps;  // slot of the token within its page
             const int i0 = e0 & (kHeadDim - 1);
             const int64_t phys = block_table[(int64_t)b * max_pages + n - 1];
-            const int64_t nrow = ((int64_t)b * num_kv_heads + hh) * kHeadDim + i0;
-            const u32x4_t kn = ld16(static_cast<const uint16_t *>(app.k_new) + nrow);
-            const int64_t crow = ((phys * num_kv_heads + hh) * ps + tok) * kHeadDim + i0;
-            if (e0 < kHeadDim)
-                st16(static_cast<uint16_t *>(app.k_cache) + crow, kn);
-            else
-                st16(static_cast<uint16_t *>(app.v_cache) + crow,
-                     ld16(static_cast<const uint16_t *>(app.v_new) + nrow));
-            // The metadata row of this page is read and written only here.
-            uint16_t *mrow = const_cast<uint16_t *>(meta) +
-                             (phys * num_kv_heads + hh) * 2 * kHeadDim + e0;
-            if (kMean) {
-                const u32x2_t k4 = *reinterpret_cast<const u32x2_t *>(
-                    static_cast<const uint16_t *>(app.k_new) + nrow - i0 + 4 * li);
-                upd = sums_with_key(tok == 0, tok == 0 ? upd : ld16(mrow), k4);
-            } else {
-                upd = meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim, tok == 0);
+            if (phys >= 0 && phys < num_phys) {  // else the page is outside the cache: no append
+                const int64_t nrow = ((int64_t)b * num_kv_heads + hh) * kHeadDim + i0;
+                const u32x4_t kn = ld16(static_cast<const uint16_t *>(app.k_new) + nrow);
+                const int64_t crow = ((phys * num_kv_heads + hh) * ps + tok) * kHeadDim + i0;
+                if (e0 < kHeadDim)
+                    st16(static_cast<uint16_t *>(app.k_cache) + crow, kn);
+                else
+                    st16(static_cast<uint16_t *>(app.v_cache) + crow,
+                         ld16(static_cast<const uint16_t *>(app.v_new) + nrow));
+                // The metadata row of this page is read and written only here.
+                uint16_t *mrow = const_cast<uint16_t *>(meta) +
+                                 (phys * num_kv_heads + hh) * 2 * kHeadDim + e0;
+                if (kMean) {
+                    const u32x2_t k4 = *reinterpret_cast<const u32x2_t *>(
+                        static_cast<const uint16_t *>(app.k_new) + nrow - i0 + 4 * li);
+                    upd = sums_with_key(tok == 0, tok == 0 ? upd : ld16(mrow), k4);
+                } else {
+                    upd = meta_with_key(tok == 0 ? kn : ld16(mrow), kn, e0 >= kHeadDim,
+                                        tok == 0);
+                }
+                st16(mrow, upd);
+                last_slot = slot;
             }
-            st16(mrow, upd);
-            last_slot = slot;
         }
     }
 
@@ -221,8 +226,9 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
             const int slot = sub + wpp * (j0 + j);
             v[j] = (u32x4_t){0u, 0u, 0u, 0u};
             if (j0 + j < my_pages && head < nh) {
-                const int64_t ph = __builtin_amdgcn_readfirstlane(s_phys[slot]);
-                v[j] = ld16_nt(mbase + ph * page_elems);
+                const int ph = __builtin_amdgcn_readfirstlane(s_phys[slot]);
+                // (an absent page reads page 0; its score is replaced by 0 when stored)
+                v[j] = ld16_nt(mbase + (int64_t)(ph < 0 ? 0 : ph) * page_elems);
             }
         }
     };
@@ -247,7 +253,9 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
         // written below instead)
         if (li < kScoreBatch && j < my_pages && head < nh &&
             !(kAppend && slot == last_slot))
-            out[slot] = kMean ? total / (float)page_tokens(page0 + slot, L, ps) : total;
+            out[slot] = s_phys[slot] < 0 ? 0.f
+                        : kMean           ? total / (float)page_tokens(page0 + slot, L, ps)
+                                          : total;
     }
     if (kAppend && last_slot >= 0) {
         // Score of the appended page from the updated slice: the same per-lane FMA chain,
@@ -505,7 +513,7 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta
     hipLaunchKernelGGL(kernel, sgrid, dim3(kScoreThreads), 0, stream,
                        static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
                        block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
-                       s.page_size, s.max_pages_per_seq, scores, app);
+                       s.page_size, s.max_pages_per_seq, s.num_phys_pages, scores, app);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
