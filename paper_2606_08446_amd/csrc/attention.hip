@@ -24,6 +24,8 @@
 //        of each, so output row m of tile c is channel 8m + c.  No LDS transpose is needed.
 //   O accumulators: lane (g, r) holds head g, channels 32r .. 32r+31 (8 tiles x 4 rows).
 // The softmax runs in the log2 domain (scale * log2(e) folded into one multiply).
+#include <atomic>
+
 #include "common.h"
 
 namespace sparrow {
@@ -494,14 +496,16 @@ __global__ __launch_bounds__(kMergeThreads) void k_attn_merge(AttnArgs a)
 }
 
 // Streaming waves on the current device: compute units x resident workgroups x 4, capped.
-// (A per-process cache of device attributes; no per-call state.)
+// (A per-process cache of device attributes, safe to fill from several host threads at
+// once - they all store the same value; no per-call state.)
 int device_waves()
 {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
         return kMaxWaves;
-    if (cached[dev] == 0) {
+    int w = cached[dev].load(std::memory_order_relaxed);
+    if (w == 0) {
         int cus = 0, per_cu = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             cus < 1)
@@ -510,10 +514,11 @@ int device_waves()
                                                          kAttnThreads, 4096) != hipSuccess ||
             per_cu < 1)
             per_cu = 1;
-        const int w = cus * per_cu * kAttnWaves;
-        cached[dev] = w < kMaxWaves ? w : kMaxWaves;
+        w = cus * per_cu * kAttnWaves;
+        w = w < kMaxWaves ? w : kMaxWaves;
+        cached[dev].store(w, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return w;
 }
 
 }  // namespace
