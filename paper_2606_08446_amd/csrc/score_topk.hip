@@ -10,8 +10,8 @@
 // with the loads laid out for fully coalesced 1 KiB reads (see the kernel).  Scores are
 // written as fp32 to the workspace; sequences whose budget covers every page are skipped.
 //
-// k_topk: one workgroup per (sequence, KV head) selects the k largest scores with ties
-// to the lower page index.  Scores become order-preserving uint32 keys in LDS; a radix
+// k_topk: one workgroup per (sequence, KV head) - 512 threads, or 256 from 1024 units on -
+// selects the k largest scores with ties to the lower page index.  Scores become order-preserving uint32 keys in LDS; a radix
 // select over 8-bit digits (from the highest bit where the keys differ, stopping as soon
 // as the selection is decided) finds the threshold T and how many keys equal to T to
 // keep; one block scan of (count > T, count == T) then places every kept page at its
@@ -26,8 +26,7 @@ constexpr int kScoreWaves = kScoreThreads / 64;
 constexpr int kScorePages = 32;  // pages per workgroup
 constexpr int kScoreBatch = 8;   // pages per load batch of a wave
 constexpr int kScoreHeads = 8;   // KV heads per workgroup (at most)
-constexpr int kTopkThreads = 512;
-constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kTopkManyUnits = 1024;  // from this many units on: 256-thread workgroups
 constexpr int kTopkBatch = 8;   // score loads in flight per thread
 
 // Sum of 8 per-lane values over the 32 lanes of a half-wave: afterwards lane i holds the
@@ -292,11 +291,13 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane)
     return x;
 }
 
+template <int kTopkThreads>
 __global__ __launch_bounds__(kTopkThreads) void k_topk(
     const float *__restrict__ scores, const int32_t *__restrict__ seq_lens, Sched sched,
     int k_max, int num_kv_heads, int ps, int max_pages, int32_t *__restrict__ out_k,
     int32_t *__restrict__ out_idx)
 {
+    constexpr int kTopkWaves = kTopkThreads / 64;
     extern __shared__ uint32_t keys[];  // [max_pages]
     __shared__ uint32_t hist[2][256];
     __shared__ uint32_t red_a[kTopkWaves], red_b[kTopkWaves], red_c[kTopkWaves];
@@ -517,7 +518,10 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_topk, dim3(units), dim3(kTopkThreads),
+    // Many units: smaller workgroups, so more of them share a CU (the per-unit work is
+    // latency-bound); few units: larger ones, so each finishes sooner.
+    const bool many = units >= kTopkManyUnits;
+    hipLaunchKernelGGL(many ? k_topk<256> : k_topk<512>, dim3(units), dim3(many ? 256 : 512),
                        (size_t)s.max_pages_per_seq * sizeof(uint32_t), stream, scores, seq_lens,
                        sched, k_max, s.num_kv_heads, s.page_size, s.max_pages_per_seq, out_k,
                        out_idx);
