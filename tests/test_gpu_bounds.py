@@ -173,3 +173,31 @@ def test_append_to_a_page_outside_the_cache_writes_nothing():
     ora_idx = oracle.select(lens, ora_k, s32, PS, k_max)
     check_indices(kf.cpu().numpy(), idxf.cpu().numpy(), ora_k, ora_idx, s32, s64, lens, PS,
                   k_max)
+
+
+def test_mean_landmark_with_absent_pages():
+    log("case mean landmark, absent pages")
+    inp, bt, n = corrupted_inputs()
+    P = inp.num_phys_pages
+    h = host(inp)
+    kz, vz, btz = oracle_view(h, P)
+    lens = h["lens"]
+    s = inp.workload.schedule
+    mean = S.SPARROW_LANDMARK_MEAN
+    sums = S.new_meta(P, HKV, DEV, landmark=mean)
+    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, sums, landmark=mean)
+    torch.cuda.synchronize()
+    ora_sums = oracle.page_key_sums(kz, btz, lens)
+    np.testing.assert_array_equal(sums.cpu().numpy().view(np.uint32),
+                                  ora_sums[:P].view(np.uint32))
+    k_max = S.budget_bound(lens, PS, s.bin_tokens, s.min_pages, s.frac_num, s.frac_den)
+    k, idx = S.page_score_topk(inp.q, sums, inp.block_table, inp.seq_lens, inp.k_cache.shape,
+                               inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, k_max,
+                               landmark=mean)
+    torch.cuda.synchronize()
+    s32, s64 = oracle.page_scores_mean(h["q"], ora_sums, btz, lens, PS)
+    ora_k = np.minimum(oracle.budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
+                                      s.frac_den), k_max).astype(np.int32)
+    ora_idx = oracle.select(lens, ora_k, s32, PS, k_max)
+    check_indices(k.cpu().numpy(), idx.cpu().numpy(), ora_k, ora_idx, s32, s64, lens, PS,
+                  k_max)
