@@ -172,9 +172,10 @@ int sparrow_page_meta_update(const sparrow_shape_t *shape, const void *k_cache,
  *     k_cache[phys][h][slot][:] = k_new[b][h][:],  v_cache[phys][h][slot][:] = v_new[b][h][:]
  * with phys = block_table[b][(L - 1) / page_size], and the page's metadata becomes the
  * channel-wise min/max of its old metadata and the new key (the key itself when the
- * slot is 0); with SPARROW_LANDMARK_MEAN its key sum plus the new key.  This equals the metadata rebuilt from the page's L - page*page_size valid
- * tokens (sparrow_page_meta_update) provided the old metadata described the tokens
- * before L - 1.  Sequences with seq_lens[b] < 1 or seq_lens[b] > max_pages_per_seq *
+ * slot is 0); with SPARROW_LANDMARK_MEAN its key sum plus the new key.  This equals
+ * the metadata rebuilt from the page's L - page*page_size valid tokens
+ * (sparrow_page_meta_update) provided the old metadata described the tokens before
+ * L - 1.  Sequences with seq_lens[b] < 1 or seq_lens[b] > max_pages_per_seq *
  * page_size are left untouched.  Sequences must use distinct physical pages.
  *
  * Arguments: shape (host); k_new, v_new (device bf16 [batch][num_kv_heads][head_dim]);
@@ -196,8 +197,8 @@ int sparrow_append_kv(const sparrow_shape_t *shape, const void *k_new, const voi
  *              sum_i max(q[b][j][i] * mn_i(p), q[b][j][i] * mx_i(p))
  * (an upper bound of q_j . k_t over the tokens of the page), with fp32
  * arithmetic; with SPARROW_LANDMARK_MEAN, S_h(p) = sum_j q_j . (sum(p) / n_valid(p)),
- * the query group against the page's mean key.  k_b is the schedule's budget (see sparrow_schedule_t), capped
- * at k_max.  The k_b pages of largest S_h are kept, ties going to the lower
+ * the query group against the page's mean key.  k_b is the schedule's budget (see
+ * sparrow_schedule_t), capped at k_max.  The k_b pages of largest S_h are kept, ties going to the lower
  * page index (-0 equals +0), and written in ascending page order to
  * out_idx[b][h][0 .. k_b); the rest of the row up to k_max is set to -1.
  * out_k[b] = k_b.  When k_b == n_b no page is scored and every page is kept.

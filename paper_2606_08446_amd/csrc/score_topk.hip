@@ -9,13 +9,14 @@
 // one vector): HBM-bound with about one flop per byte, so it runs on VALU FMAs in fp32,
 // with the loads laid out for fully coalesced 1 KiB reads (see the kernel).  Scores are
 // written as fp32 to the workspace; sequences whose budget covers every page are skipped.
+// A page whose block-table entry lies outside the cache is absent: score 0, nothing read.
 //
 // k_topk: one workgroup per (sequence, KV head) - 512 threads, or 256 from 1024 units on -
-// selects the k largest scores with ties to the lower page index.  Scores become order-preserving uint32 keys in LDS; a radix
-// select over 8-bit digits (from the highest bit where the keys differ, stopping as soon
-// as the selection is decided) finds the threshold T and how many keys equal to T to
-// keep; one block scan of (count > T, count == T) then places every kept page at its
-// rank in ascending page order.
+// selects the k largest scores with ties to the lower page index.  Scores become
+// order-preserving uint32 keys in LDS; a radix select over 8-bit digits (from the highest
+// bit where the keys differ, stopping as soon as the selection is decided) finds the
+// threshold T and how many keys equal to T to keep; one block scan of (count > T,
+// count == T) then places every kept page at its rank in ascending page order.
 #include "common.h"
 
 namespace sparrow {
