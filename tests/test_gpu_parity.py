@@ -74,6 +74,43 @@ def test_small_sweep(case):
     full_check(inp)
 
 
+
+# ------------------------------------------------------------------- seeded random shapes
+def random_case(seed):
+    """A shape drawn from a seeded generator: group size, KV heads, page size, ragged
+    lengths (0 and 1 included now and then) and one of the schedule forms."""
+    rng = np.random.default_rng(9000 + seed)
+    G = int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
+    Hkv = int(rng.integers(1, 13))
+    ps = int(rng.choice([16, 32, 64, 128]))
+    B = int(rng.integers(1, 7))
+    lengths = [int(x) for x in rng.integers(0, 9000, size=B)]
+    if rng.random() < 0.3:
+        lengths[int(rng.integers(0, B))] = int(rng.choice([0, 1, ps, ps + 1]))
+    form = int(rng.integers(0, 3))
+    if form == 0:
+        sched = W.fixed_budget(int(rng.integers(1, 40)))
+    elif form == 1:
+        sched = W.fraction_budget(int(rng.integers(1, 5)), int(rng.integers(5, 20)),
+                                  floor_pages=int(rng.integers(0, 6)))
+    else:
+        sched = W.rising_permille(2048, 2048, 8192, int(rng.integers(20, 100)),
+                                  int(rng.integers(100, 400)))
+    return G, Hkv, ps, tuple(lengths), sched
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_shapes(seed):
+    G, Hkv, ps, lengths, sched = random_case(seed)
+    log(f"case random {seed}: G={G} Hkv={Hkv} ps={ps} lens={lengths}")
+    inp = small_inputs(G, Hkv, ps, lengths, seed=700 + seed, schedule=sched)
+    s = inp.workload.schedule
+    k_max = S.budget_bound(inp.lens_host, ps, s.bin_tokens, s.min_pages, s.frac_num, s.frac_den)
+    if seed % 4 == 3:
+        k_max = max(1, k_max // 2)  # a k_max below some budgets: the cap applies
+    full_check(inp, k_max=k_max)
+
+
 @pytest.mark.parametrize("k_pages", ["one", "n_minus_1", "n", "more"])
 def test_budget_edges(k_pages):
     lengths = (800, 801, 3000)
