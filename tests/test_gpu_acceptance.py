@@ -50,6 +50,28 @@ def test_acceptance_matches_oracle(dtype, V, tau):
         np.testing.assert_allclose(got.cpu().numpy(), 1.0, rtol=0, atol=2e-6)
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_acceptance_random_shapes(seed):
+    """Seeded random vocabulary sizes, token counts, temperatures and dtypes, with rows
+    that start off a 16-byte boundary on odd seeds."""
+    rng = np.random.default_rng(6000 + seed)
+    dtype = "bf16" if seed % 4 >= 2 else "f32"
+    T = int(rng.integers(1, 40))
+    V = int(rng.integers(1, 20000))
+    tau = 0.0 if seed == 5 else float(rng.uniform(0.2, 2.0))
+    off = int(rng.integers(1, 8 if dtype == "bf16" else 4)) if seed % 2 else 0
+    log(f"case acceptance random {seed}: {dtype} T={T} V={V} tau={tau:.3f} offset={off}")
+    li = W.generate_logits(W.small_logits(T=T + 1, V=V, seed=60 + seed, dtype=dtype), DEV)
+    t = li.target.view(-1)[off:off + T * V].view(T, V)
+    d = li.draft.view(-1)[off:off + T * V].view(T, V)
+    got = S.acceptance_rate(t, d, tau)
+    torch.cuda.synchronize()
+    ref = oracle.acceptance(host_rows(t), host_rows(d), tau)
+    err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+    log(f"  max abs err {err.max():.2e}")
+    assert err.max() <= ALPHA_TOL
+
+
 def test_acceptance_unaligned_row_starts():
     # views whose rows start off a 16-byte boundary (both rows in the same phase)
     li = W.generate_logits(W.small_logits(T=9, V=2051, seed=4), DEV)

@@ -112,8 +112,29 @@ def test_fused_equals_append_then_select(case):
     G, Hkv, ps, lengths = CASES[case]
     log(f"case fused G={G} Hkv={Hkv} ps={ps} lengths={lengths}")
     # a quarter of the pages with a floor of 2 pages: short sequences are dense (k = n)
-    inp, meta, meta0, kn, vn = append_case(G, Hkv, ps, lengths, seed=60 + case,
-                                           schedule=W.Schedule(1 << 20, (2,), (1,), 4))
+    fused_check(G, Hkv, ps, lengths, 60 + case, W.Schedule(1 << 20, (2,), (1,), 4))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_fused_random_shapes(seed):
+    rng = np.random.default_rng(5000 + seed)
+    G = int(rng.choice([1, 2, 4, 5, 8]))
+    Hkv = int(rng.integers(1, 11))
+    ps = int(rng.choice([16, 32, 64, 128]))
+    B = int(rng.integers(1, 7))
+    lengths = [int(x) for x in rng.integers(1, 6000, size=B)]
+    lengths[int(rng.integers(0, B))] = int(rng.choice([1, ps, ps + 1, 2 * ps]))
+    sched = W.fraction_budget(int(rng.integers(1, 4)), int(rng.integers(4, 12)),
+                              floor_pages=int(rng.integers(0, 4)))
+    log(f"case fused random {seed}: G={G} Hkv={Hkv} ps={ps} lengths={lengths}")
+    fused_check(G, Hkv, ps, tuple(lengths), 5100 + seed, sched, skip_last=seed % 2 == 0)
+
+
+def fused_check(G, Hkv, ps, lengths, seed, schedule, skip_last=True):
+    """The fused append + selection equals the append followed by the selection bit for
+    bit, and both match the oracle through attention."""
+    inp, meta, meta0, kn, vn = append_case(G, Hkv, ps, lengths, seed=seed, schedule=schedule,
+                                           skip_last=skip_last)
     k_max = inp.max_pages
     a = clone_inputs(inp)
     meta_a = meta.clone()
