@@ -146,13 +146,18 @@ struct Cursor {
 struct Batch {
     int b, h, j0, n, L;
     bool ends_unit;
-    int phys;  // physical page (-1: entry outside the sequence or the cache)
+    int lp;    // logical page (-1: none)
+    int phys;  // physical page, as the block table gives it (checked when used)
     int tok0;  // first token of the page
 };
 
+// A page-list batch is fetched in two phases so that no wait on its loads drains the K/V
+// loads in flight (a wave's loads complete in order): fetch_batch_begin issues the index
+// loads and advances the cursor; fetch_batch_end, called one chunk later, when the
+// indices have arrived, issues the block-table loads, which are consumed a batch later.
 template <bool kSparse>
-__device__ __forceinline__ void fetch_batch(const AttnArgs &a, const int32_t *s_off, Cursor &c,
-                                            int64_t pos_end, Batch &t, int lane)
+__device__ __forceinline__ void fetch_batch_begin(const AttnArgs &a, const int32_t *s_off,
+                                                  Cursor &c, int64_t pos_end, Batch &t, int lane)
 {
     const int Hkv = a.num_kv_heads;
     t.b = c.b;
@@ -167,18 +172,9 @@ __device__ __forceinline__ void fetch_batch(const AttnArgs &a, const int32_t *s_
     t.n = n;
     t.ends_unit = c.j + n == c.cnt;
     t.L = clamp_len(a.seq_lens[c.b], a.ps, a.max_pages);
-    const int np = (t.L + a.ps - 1) / a.ps;
-    t.phys = -1;
-    t.tok0 = 0;
-    if (lane < n) {
-        const int lp = kSparse ? a.idx[((int64_t)c.b * Hkv + c.h) * a.k_max + c.j + lane]
-                               : c.j + lane;
-        if (lp >= 0 && lp < np) {
-            const int pp = a.block_table[(int64_t)c.b * a.max_pages + lp];
-            t.phys = pp >= 0 && pp < a.num_phys ? pp : -1;  // outside the cache: absent
-        }
-        t.tok0 = lp * a.ps;
-    }
+    t.lp = -1;
+    if (lane < n)
+        t.lp = kSparse ? a.idx[((int64_t)c.b * Hkv + c.h) * a.k_max + c.j + lane] : c.j + lane;
     c.pos += n;
     c.j += n;
     if (c.j == c.cnt && c.pos < pos_end) {  // next unit with pages
@@ -190,6 +186,17 @@ __device__ __forceinline__ void fetch_batch(const AttnArgs &a, const int32_t *s_
             } while (s_off[c.b + 1] == s_off[c.b]);
         }
         c.cnt = s_off[c.b + 1] - s_off[c.b];
+    }
+}
+
+__device__ __forceinline__ void fetch_batch_end(const AttnArgs &a, Batch &t)
+{
+    const int np = (t.L + a.ps - 1) / a.ps;
+    t.phys = -1;
+    t.tok0 = 0;
+    if (t.lp >= 0 && t.lp < np) {  // entries outside the sequence: no page
+        t.phys = a.block_table[(int64_t)t.b * a.max_pages + t.lp];
+        t.tok0 = t.lp * a.ps;
     }
 }
 
@@ -256,10 +263,12 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
     }
 
     Batch bc, bn;
-    fetch_batch<kSparse>(a, s_off, cur, pos_end, bc, lane);
+    fetch_batch_begin<kSparse>(a, s_off, cur, pos_end, bc, lane);
+    fetch_batch_end(a, bc);
     bool have_next = cur.pos < pos_end;
+    bool bn_pending = have_next;  // bn's block-table loads not issued yet
     if (have_next)
-        fetch_batch<kSparse>(a, s_off, cur, pos_end, bn, lane);
+        fetch_batch_begin<kSparse>(a, s_off, cur, pos_end, bn, lane);
 
     bf16x8_t qf[4], qn[4];
     load_q(a, bc.b, bc.h, lr, lg, qf);
@@ -278,7 +287,8 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
         const int sub = ci - pi * cpp;
         const int ph = __builtin_amdgcn_readlane(t.phys, pi);
         tok = __builtin_amdgcn_readlane(t.tok0, pi) + 16 * sub;
-        const bool live = ph >= 0 && tok < t.L;
+        // a block-table entry outside the cache is an absent page
+        const bool live = ph >= 0 && ph < a.num_phys && tok < t.L;
         if (live) {
             const int64_t off =
                 ((int64_t)ph * Hkv + t.h) * head_elems + (int64_t)(16 * sub) * kHeadDim;
@@ -299,7 +309,15 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
         const bool last_in_batch = ci + 1 == bc.n * cpp;
         if (!last_in_batch) {
             live_next = issue(bc, ci + 1, nxt, tok_next);
+            if (bn_pending) {
+                fetch_batch_end(a, bn);
+                bn_pending = false;
+            }
         } else if (have_next) {
+            if (bn_pending) {  // a one-chunk batch: bn is needed now
+                fetch_batch_end(a, bn);
+                bn_pending = false;
+            }
             live_next = issue(bn, 0, nxt, tok_next);
             if (bc.ends_unit)
                 load_q(a, bn.b, bn.h, lr, lg, qn);
@@ -404,8 +422,9 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
         bc = bn;
         ci = 0;
         have_next = cur.pos < pos_end;
+        bn_pending = have_next;
         if (have_next)
-            fetch_batch<kSparse>(a, s_off, cur, pos_end, bn, lane);
+            fetch_batch_begin<kSparse>(a, s_off, cur, pos_end, bn, lane);
     }
 }
 
