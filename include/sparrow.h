@@ -204,12 +204,12 @@ int sparrow_append_kv(const sparrow_shape_t *shape, const void *k_new, const voi
  * out_k[b] = k_b.  When k_b == n_b no page is scored and every page is kept.
  *
  * Arguments: shape (host); q, meta, block_table, seq_lens (device);
- * schedule (host struct with device tables); k_max >= 1 (the row length of
- * out_idx; callers pass at least the largest budget); out_k (device [batch]);
+ * schedule (host struct with device tables); 1 <= k_max <= SPARROW_MAX_PAGES_PER_SEQ
+ * (the row length of out_idx; callers pass at least the largest budget); out_k (device [batch]);
  * out_idx (device [batch][num_kv_heads][k_max]); workspace of at least
  * sparrow_workspace_size(shape, k_max, SPARROW_OP_SCORE_TOPK) bytes (device,
  * contents need not be initialised); stream.
- * Errors: SPARROW_EINVAL (null pointers, k_max < 1, bad schedule sizes or negative
+ * Errors: SPARROW_EINVAL (null pointers, k_max out of range, bad schedule sizes or negative
  * forced-page counts), SPARROW_EUNSUPPORTED, SPARROW_EWORKSPACE, SPARROW_EHIP.
  */
 int sparrow_page_score_topk(const sparrow_shape_t *shape, const void *q, const void *meta,
@@ -247,7 +247,8 @@ int sparrow_append_score_topk(const sparrow_shape_t *shape, const void *q, const
  * row.  out_dtype is SPARROW_OUT_F32 or SPARROW_OUT_BF16.
  *
  * Arguments: shape (host); q, k_cache, v_cache, block_table, seq_lens, k
- * (device [batch]), idx (device [batch][num_kv_heads][k_max]); k_max >= 1;
+ * (device [batch]), idx (device [batch][num_kv_heads][k_max]);
+ * 1 <= k_max <= SPARROW_MAX_PAGES_PER_SEQ;
  * scale (typically 1/sqrt(head_dim)); out (device, written); out_dtype;
  * workspace of at least sparrow_workspace_size(shape, k_max,
  * SPARROW_OP_SPARSE_ATTN) bytes; stream.

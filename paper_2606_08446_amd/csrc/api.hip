@@ -94,7 +94,7 @@ static int score_topk_call(const sparrow_shape_t *shape, const void *q, void *me
     if (!al16(q) || !al16(meta) || !al4(block_table) || !al4(seq_lens) || !al4(out_k) ||
         !al4(out_idx) || !al16(workspace))
         return SPARROW_EINVAL;
-    if (k_max < 1 || schedule->bin_tokens < 1 || schedule->n_bins < 1 || schedule->frac_den < 1 ||
+    if (k_max < 1 || k_max > SPARROW_MAX_PAGES_PER_SEQ || schedule->bin_tokens < 1 || schedule->n_bins < 1 || schedule->frac_den < 1 ||
         !schedule->min_pages || !schedule->frac_num || schedule->sink_pages < 0 ||
         schedule->local_pages < 0)
         return SPARROW_EINVAL;
@@ -157,7 +157,7 @@ int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, cons
     if (!al16(q) || !al16(k_cache) || !al16(v_cache) || !al4(block_table) || !al4(seq_lens) ||
         !al4(k) || !al4(idx) || !al16(out) || !al16(workspace))
         return SPARROW_EINVAL;
-    if (k_max < 1)
+    if (k_max < 1 || k_max > SPARROW_MAX_PAGES_PER_SEQ)
         return SPARROW_EINVAL;
     if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
         return SPARROW_EUNSUPPORTED;
@@ -263,7 +263,9 @@ size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32
     switch (op) {
     case SPARROW_OP_SCORE_TOPK: return shape->batch > kMaxBatch ? 0 : score_topk_workspace(*shape);
     case SPARROW_OP_SPARSE_ATTN:
-        return k_max < 1 || shape->batch > kMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
+        return k_max < 1 || k_max > SPARROW_MAX_PAGES_PER_SEQ || shape->batch > kMaxBatch
+                   ? 0
+                   : plan_attention(*shape).workspace_bytes;
     case SPARROW_OP_DENSE_ATTN:
         return shape->batch > kMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
     default: return 0;

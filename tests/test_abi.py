@@ -159,6 +159,13 @@ def test_null_shape_and_schedule_are_rejected(lib):
     assert call("fused", good_shape(), sched=S.Schedule(2048, 1, FAKE, None, 10)) == \
         S.SPARROW_EINVAL
     assert call("sparse", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    # no budget exceeds the largest page count, so a longer row is refused
+    big = S.SPARROW_MAX_PAGES_PER_SEQ + 1
+    for fn in ("topk", "fused", "sparse"):
+        assert call(fn, good_shape(), k_max=big) == S.SPARROW_EINVAL
+        assert call(fn, good_shape(), k_max=2**31 - 1) == S.SPARROW_EINVAL
+    assert call("topk", good_shape(), k_max=S.SPARROW_MAX_PAGES_PER_SEQ, ws_bytes=0) == \
+        S.SPARROW_EWORKSPACE
 
 
 def test_unsupported_output_dtype(lib):
@@ -189,6 +196,8 @@ def test_workspace_size_properties(lib):
     assert S.sparrow_workspace_size(shape, 8, 99) == 0
     assert S.sparrow_workspace_size(good_shape(page_size=8), 8, 0) == 0
     assert S.sparrow_workspace_size(shape, 0, S.SPARROW_OP_SPARSE_ATTN) == 0
+    assert S.sparrow_workspace_size(shape, S.SPARROW_MAX_PAGES_PER_SEQ + 1,
+                                    S.SPARROW_OP_SPARSE_ATTN) == 0
     a = S.sparrow_workspace_size(shape, 8, S.SPARROW_OP_SPARSE_ATTN)
     b = S.sparrow_workspace_size(shape, 64, S.SPARROW_OP_SPARSE_ATTN)
     assert 0 < a <= b
