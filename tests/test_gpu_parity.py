@@ -63,6 +63,11 @@ SWEEP = [
     (1, 9, 16, (3000, 17, 900), W.fraction_budget(1, 5)),
     (2, 12, 32, (5000, 64, 1), W.fraction_budget(1, 4)),
     (3, 5, 16, (2048, 2049, 333), W.fraction_budget(1, 3)),
+    # the remaining group sizes up to 16 that no case above uses: some query-head rows of
+    # the padded 16-row MFMA tile unused, and group sums of more heads in the scoring
+    (6, 3, 64, (4000, 129, 7000), W.fraction_budget(1, 4)),
+    (7, 2, 128, (2600, 257), W.fraction_budget(1, 2)),
+    (12, 1, 32, (6000, 31, 1900), W.rising_permille(2048, 2048, 8192, 40, 200)),
 ]
 
 
