@@ -18,6 +18,7 @@
 // threshold T and how many keys equal to T to keep; one block scan of (count > T,
 // count == T) then places every kept page at its rank in ascending page order.
 #include "common.h"
+#include "wave.h"
 
 namespace sparrow {
 namespace {
@@ -281,17 +282,6 @@ __device__ __forceinline__ uint32_t score_key(float s)
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane)
-{
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t t = __shfl_up(x, d, 64);
-        if (lane >= d)
-            x += t;
-    }
-    return x;
-}
-
 template <int kTopkThreads>
 __global__ __launch_bounds__(kTopkThreads) void k_topk(
     const float *__restrict__ scores, const int32_t *__restrict__ seq_lens, Sched sched,
@@ -356,11 +346,8 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
     }
     for (int t = tid; t < 256; t += kTopkThreads)
         hist[0][t] = 0u;
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
-        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, d, 64));
-    }
+    kmin = wave_min(kmin);
+    kmax = wave_max(kmax);
     if (lane == 0) {
         red_a[wave] = kmin;
         red_b[wave] = kmax;
@@ -411,7 +398,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
                 const uint32_t c0 = hist[cur][255 - 4 * lane], c1 = hist[cur][254 - 4 * lane];
                 const uint32_t c2 = hist[cur][253 - 4 * lane], c3 = hist[cur][252 - 4 * lane];
                 const uint32_t tot = c0 + c1 + c2 + c3;
-                const uint32_t incl = wave_inclusive_scan(tot, lane);
+                const uint32_t incl = wave_scan_add(tot);
                 uint32_t acc = incl - tot;  // keys with a larger digit
                 if (acc < rem && rem <= incl) {
                     int d;
@@ -466,7 +453,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         eq += key == T;
     }
     const uint32_t packed = (gt << 16) | eq;  // n <= 15360 < 2^16
-    uint32_t incl = wave_inclusive_scan(packed, lane);
+    uint32_t incl = wave_scan_add(packed);
     if (lane == 63)
         red_c[wave] = incl;
     __syncthreads();
