@@ -144,7 +144,7 @@ def acceptance_traffic(workload_name):
     return None if v is None else float(v)
 
 
-def source_sha(files=("attention.hip", "common.h")):
+def source_sha(files=("attention.hip", "common.h", "wave.h")):
     import hashlib
     h = hashlib.sha256()
     for f in files:

@@ -27,6 +27,7 @@
 #include <atomic>
 
 #include "common.h"
+#include "wave.h"
 
 namespace sparrow {
 namespace {
@@ -114,13 +115,7 @@ __device__ void seq_prefix(const AttnArgs &a, int32_t *s_off, int32_t *s_tmp)
     int local = 0;
     for (int b = b0; b < b1; ++b)
         local += list_pages<kSparse>(a, b);
-    int incl = local;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int t = __shfl_up(incl, d, 64);
-        if (lane >= d)
-            incl += t;
-    }
+    const int incl = (int)wave_scan_add((uint32_t)local);  // totals < 2^31 (max batch x pages)
     if (lane == 63)
         s_tmp[wave] = incl;
     __syncthreads();
@@ -243,16 +238,19 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
     const int64_t head_elems = (int64_t)ps * kHeadDim;
 
     // Locate the first position: the last sequence whose offset is <= pos_begin is the one
-    // holding it (empty sequences before it share its offset).
+    // holding it (empty sequences before it share its offset).  The offsets do not decrease,
+    // so a wave narrows [lo, lo + span) 64-fold per round: lane l tests entry lo + l step,
+    // and the number of lanes that pass gives the last entry <= pos_begin (s_off[lo] always
+    // is).
     Cursor cur;
     {
-        int lo = 0, hi = B - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if ((int64_t)s_off[mid] * Hkv <= pos_begin)
-                lo = mid;
-            else
-                hi = mid - 1;
+        int lo = 0, span = B;
+        while (span > 1) {
+            const int step = (span + 63) >> 6;
+            const bool ok = lane * step < span && (int64_t)s_off[lo + lane * step] * Hkv <= pos_begin;
+            const int t = __popcll(__ballot(ok)) - 1;
+            lo += t * step;
+            span = min(step, span - t * step);
         }
         cur.b = lo;
         cur.cnt = s_off[lo + 1] - s_off[lo];
