@@ -431,7 +431,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
 // lane) per query-head row, 8 rows per 256-thread workgroup, no LDS.  Segments are taken
 // kMergeChunk at a time: every lane issues the loads of its channels for the whole chunk at
 // once while lane t loads the (m, l) pair of segment t; the weights 2^(m - M) against the
-// running maximum M are formed with half-wave shuffles.
+// running maximum M are formed with half-wave DPP reductions and lane reads.
 constexpr int kMergeChunk = 16;
 constexpr int kMergeThreads = 256;
 constexpr int kMergeRows = kMergeThreads / 32;
@@ -489,24 +489,21 @@ __global__ __launch_bounds__(kMergeThreads) void k_attn_merge(AttnArgs a)
             m = a.ml_part[sg * 2];
             l = a.ml_part[sg * 2 + 1];
         }
-        float cm = m;
-#pragma unroll
-        for (int x = 1; x < 32; x <<= 1)
-            cm = fmaxf(cm, __shfl_xor(cm, x, 64));
+        const float cm = half_wave_max(m);
         const float Mn = fmaxf(M, cm);
         const float r = M == -INFINITY ? 0.f : exp2f(M - Mn);
         const float f = m == -INFINITY ? 0.f : exp2f(m - Mn);  // no valid pages: weight 0
-        float fl = f * l;
-#pragma unroll
-        for (int x = 1; x < 32; x <<= 1)
-            fl += __shfl_xor(fl, x, 64);
+        const float fl = half_wave_sum(f * l);
         lsum = lsum * r + fl;
         M = Mn;
         acc *= r;
-        const int base = threadIdx.x & 32;  // first lane of this half-wave
+        const bool upper = threadIdx.x & 32;  // this half-wave's weights sit in lanes 32..
 #pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i)
-            acc += __shfl(f, base + i, 64) * o[i];
+        for (int i = 0; i < kMergeChunk; ++i) {
+            const float f_lo = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), i));
+            const float f_hi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 32 + i));
+            acc += (upper ? f_hi : f_lo) * o[i];
+        }
     }
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
     store_out4(a.out, a.out_bf16, orow, acc * inv);

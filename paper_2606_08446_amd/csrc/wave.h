@@ -62,4 +62,37 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t x)
     return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
+// Reduction over each 32-lane half of the wave with the associative, commutative `op` on
+// fp32: the row scan, then row_bcast:15 adds row 0 into row 1 and row 2 into row 3, so
+// lanes 31 and 63 hold the two halves' results.  Every lane gets its own half's.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_move_f(float x, float identity)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(identity), __float_as_int(x),
+                                                      kCtrl, kRowMask, 0xf, false));
+}
+
+template <typename Op>
+__device__ __forceinline__ float half_wave_reduce(float x, float identity, Op op)
+{
+    x = op(x, dpp_move_f<kDppRowShr1, 0xf>(x, identity));
+    x = op(x, dpp_move_f<kDppRowShr2, 0xf>(x, identity));
+    x = op(x, dpp_move_f<kDppRowShr4, 0xf>(x, identity));
+    x = op(x, dpp_move_f<kDppRowShr8, 0xf>(x, identity));
+    x = op(x, dpp_move_f<kDppRowBcast15, 0xa>(x, identity));
+    const float lo = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 31));
+    const float hi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+    return (threadIdx.x & 32) ? hi : lo;
+}
+
+__device__ __forceinline__ float half_wave_max(float x)
+{
+    return half_wave_reduce(x, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+}
+
+__device__ __forceinline__ float half_wave_sum(float x)
+{
+    return half_wave_reduce(x, 0.f, [](float a, float b) { return a + b; });
+}
+
 }  // namespace sparrow
