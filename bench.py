@@ -111,6 +111,29 @@ def dense_bytes(inp, lens):
         B * w.num_q_heads * 128 * (2 + 4) + B * w.num_kv_heads * 4 * 128 * 2
 
 
+def copy_bandwidth(stream):
+    """Read + write bytes per second of a plain 1 GiB device-to-device copy (the runtime's
+    copy kernel): a practical streaming reference beside the 8 TB/s peak."""
+    import torch
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    reps = 5
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return round(2 * n / (ms * 1e-3) / 1e9, 1)
+
+
 def read_traffic(kernel_src_sha, workload_name):
     """HBM traffic per launch from the committed counter summary, if it was taken on this
     workload with the current attention source."""
@@ -484,6 +507,7 @@ def main():
     dominant = max(phase, key=phase.get)
     dom_gbps = by[dominant] / (phase[dominant] * 1e-3) / 1e9
     traffic = read_traffic(source_sha(), w.name) if dominant == "sparse_attn" else None
+    copy_gbps = copy_bandwidth(stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -521,6 +545,7 @@ def main():
                            "; one token appended per sequence per step"},
         "achieved_GBps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "measured_copy_GBps": copy_gbps,
         "algorithmic_bytes_per_step": {k: int(v) for k, v in by.items()},
         "phase_ms": {k: round(v, 5) for k, v in phase.items()},
         "dense": {"queries_per_s": round(B * L_layers / (ms_dense * 1e-3), 2),
