@@ -118,19 +118,21 @@ __device__ __forceinline__ int clamp_len(int L, int ps, int max_pages)
     return L < 0 ? 0 : (L > cap ? cap : L);
 }
 
-// Page budget of a sequence of L tokens from the schedule, capped at k_max.
-__device__ __forceinline__ int budget_pages(int L, int ps, const Sched &s, int k_max)
+// Schedule bin of a sequence of L >= 1 tokens (the position of its last token).
+__device__ __forceinline__ int budget_bin(int L, const Sched &s)
 {
-    if (L <= 0)
-        return 0;
+    const int bin = (L - 1) / s.bin_tokens;
+    return bin > s.n_bins - 1 ? s.n_bins - 1 : bin;
+}
+
+// Page budget of a sequence of L >= 1 tokens from its bin's table entries, capped at k_max.
+__device__ __forceinline__ int budget_from(int L, int ps, int32_t min_pages, int32_t frac_num,
+                                           int32_t frac_den, int k_max)
+{
     const int64_t n = (L + ps - 1) / ps;
-    int bin = (L - 1) / s.bin_tokens;
-    if (bin > s.n_bins - 1)
-        bin = s.n_bins - 1;
-    int64_t k = (n * (int64_t)s.frac_num[bin] + s.frac_den - 1) / s.frac_den;
-    const int64_t floor_pages = s.min_pages[bin];
-    if (k < floor_pages)
-        k = floor_pages;
+    int64_t k = (n * (int64_t)frac_num + frac_den - 1) / frac_den;
+    if (k < min_pages)
+        k = min_pages;
     if (k < 1)
         k = 1;
     if (k > n)
@@ -138,6 +140,15 @@ __device__ __forceinline__ int budget_pages(int L, int ps, const Sched &s, int k
     if (k > k_max)
         k = k_max;
     return (int)k;
+}
+
+// Page budget of a sequence of L tokens from the schedule, capped at k_max.
+__device__ __forceinline__ int budget_pages(int L, int ps, const Sched &s, int k_max)
+{
+    if (L <= 0)
+        return 0;
+    const int bin = budget_bin(L, s);
+    return budget_from(L, ps, s.min_pages[bin], s.frac_num[bin], s.frac_den, k_max);
 }
 
 // ---------------------------------------------------------------------------------------------

@@ -109,17 +109,12 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     float *__restrict__ scores, AppendArgs app)
 {
     __shared__ int32_t s_phys[kScorePages];
+    __shared__ int32_t s_tab[2][kScoreThreads];  // the schedule's tables, when they fit
 
     const int b = blockIdx.y;
     const int h0 = blockIdx.z * kScoreHeads;
     const int nh = min(kScoreHeads, num_kv_heads - h0);
-    const int L_raw = seq_lens[b];
-    const int L = clamp_len(L_raw, ps, max_pages);
-    const int n = (L + ps - 1) / ps;
     const int page0 = blockIdx.x * kScorePages;
-    if (page0 >= n)
-        return;
-    const int npg = min(kScorePages, n - page0);
     const int G = num_q_heads / num_kv_heads;
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -127,11 +122,6 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const int half = lane >> 5;
     const int li = lane & 31;
     const int e0 = 8 * li;  // first element of this lane in the [mn | mx] row
-
-    if (tid < npg) {  // -1: an entry outside the cache, an absent page (score 0)
-        const int pp = block_table[(int64_t)b * max_pages + page0 + tid];
-        s_phys[tid] = pp >= 0 && pp < num_phys ? pp : -1;
-    }
 
     // Wave -> (head pair, page subset).
     const int npairs = (nh + 1) >> 1;
@@ -142,37 +132,36 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     const bool active = sub < wpp;
     const bool lane_on = active && head < nh;
 
-    // Weights: 8 consecutive elements of Q- (mn half) or Q+ (mx half) of this lane's head;
-    // with the mean landmark, channels 4 li .. 4 li + 3 of the group's summed queries (the
-    // lane's 16 bytes of the row are 4 fp32 key sums).
-    float w[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-        w[j] = 0.f;
-    if (kMean && lane_on) {
-        const uint16_t *qh =
-            q + ((int64_t)b * num_q_heads + (int64_t)(h0 + head) * G) * kHeadDim + 4 * li;
-        for (int g = 0; g < G; ++g) {
-            const u32x2_t v = *reinterpret_cast<const u32x2_t *>(qh + g * kHeadDim);
-            w[0] += bf16_lo(v[0]);
-            w[1] += bf16_hi(v[0]);
-            w[2] += bf16_lo(v[1]);
-            w[3] += bf16_hi(v[1]);
-        }
-    } else if (lane_on) {
-        const int i0 = e0 & (kHeadDim - 1);
-        const bool neg = e0 < kHeadDim;
-        const uint16_t *qh = q + ((int64_t)b * num_q_heads + (int64_t)(h0 + head) * G) * kHeadDim + i0;
-        for (int g = 0; g < G; ++g) {
-            const u32x4_t v = ld16(qh + g * kHeadDim);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float x0 = bf16_lo(v[j]), x1 = bf16_hi(v[j]);
-                w[2 * j] += neg ? fminf(x0, 0.f) : fmaxf(x0, 0.f);
-                w[2 * j + 1] += neg ? fminf(x1, 0.f) : fmaxf(x1, 0.f);
-            }
-        }
+    // The length, this block's block-table entries and the schedule's tables are requested
+    // together (the last two before the length is known); the queries go out right behind
+    // the first batch of metadata, so a workgroup past the end of its sequence leaves after
+    // one round trip.
+    const int L_raw = seq_lens[b];
+    int32_t pp = -1;
+    if (tid < kScorePages && page0 + tid < max_pages)
+        pp = block_table[(int64_t)b * max_pages + page0 + tid];
+    const bool tab_lds = sched.n_bins <= kScoreThreads;
+    int32_t t_min = 0, t_frac = 0;
+    if (tab_lds && tid < sched.n_bins) {
+        t_min = sched.min_pages[tid];
+        t_frac = sched.frac_num[tid];
     }
+    // (stored before the length arrives, so the compiler keeps these loads beside it; slots
+    // past the sequence's last page are never read)
+    if (tid < kScorePages)  // -1: an entry outside the cache, an absent page (score 0)
+        s_phys[tid] = pp >= 0 && pp < num_phys ? pp : -1;
+    if (tab_lds && tid < sched.n_bins) {
+        s_tab[0][tid] = t_min;
+        s_tab[1][tid] = t_frac;
+    }
+    const int L = clamp_len(L_raw, ps, max_pages);
+    const int n = (L + ps - 1) / ps;
+    if (page0 >= n)
+        return;
+    const int npg = min(kScorePages, n - page0);
+    __syncthreads();
+    const int i0 = e0 & (kHeadDim - 1);
+
     // Append of the token being decoded (position L - 1, on the last page n - 1).
     int last_slot = -1;  // slot of the appended page in this workgroup, for this lane
     u32x4_t upd = {0u, 0u, 0u, 0u};
@@ -181,9 +170,8 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
         if (slot < npg && active && sub == slot % wpp && head < nh) {
             const int hh = h0 + head;
             const int tok = L - 1 - (n - 1) * ps;  // slot of the token within its page
-            const int i0 = e0 & (kHeadDim - 1);
-            const int64_t phys = block_table[(int64_t)b * max_pages + n - 1];
-            if (phys >= 0 && phys < num_phys) {  // else the page is outside the cache: no append
+            const int64_t phys = s_phys[slot];
+            if (phys >= 0) {  // else the page is outside the cache: no append
                 const int64_t nrow = ((int64_t)b * num_kv_heads + hh) * kHeadDim + i0;
                 const u32x4_t kn = ld16(static_cast<const uint16_t *>(app.k_new) + nrow);
                 const int64_t crow = ((phys * num_kv_heads + hh) * ps + tok) * kHeadDim + i0;
@@ -210,11 +198,16 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     }
 
     // Only now is the budget needed to decide whether this sequence is scored at all.
-    if (budget_pages(L, ps, sched, k_max) >= n)
-        return;  // every page is kept: nothing to score
-    __syncthreads();
-    if (!active)
-        return;
+    int budget;
+    if (tab_lds) {
+        const int bin = L > 0 ? budget_bin(L, sched) : 0;
+        budget = L > 0 ? budget_from(L, ps, s_tab[0][bin], s_tab[1][bin], sched.frac_den, k_max)
+                       : 0;
+    } else {
+        budget = budget_pages(L, ps, sched, k_max);
+    }
+    if (budget >= n || !active)
+        return;  // every page is kept: nothing to score (or an idle wave)
 
     const int64_t page_elems = (int64_t)num_kv_heads * 2 * kHeadDim;
     const uint16_t *mbase = meta + (int64_t)(h0 + head) * 2 * kHeadDim + e0;
@@ -236,6 +229,55 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
 
     u32x4_t nxt[kScoreBatch];
     load_batch(0, nxt);
+    // Weights: 8 consecutive elements of Q- (mn half) or Q+ (mx half) of this lane's head;
+    // with the mean landmark, channels 4 li .. 4 li + 3 of the group's summed queries (the
+    // lane's 16 bytes of the row are 4 fp32 key sums).  Up to 8 query rows are requested
+    // together, then added in head order.
+    float w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        w[j] = 0.f;
+    const uint16_t *qh = q + ((int64_t)b * num_q_heads + (int64_t)(h0 + head) * G) * kHeadDim +
+                         (kMean ? 4 * li : i0);
+    auto add_rows = [&](int g0) {
+        u32x4_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            v[u] = (u32x4_t){0u, 0u, 0u, 0u};
+            if (lane_on && g0 + u < G) {
+                if (kMean) {
+                    const u32x2_t x =
+                        *reinterpret_cast<const u32x2_t *>(qh + (g0 + u) * kHeadDim);
+                    v[u][0] = x[0];
+                    v[u][1] = x[1];
+                } else {
+                    v[u] = ld16(qh + (g0 + u) * kHeadDim);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (!(lane_on && g0 + u < G))
+                continue;
+            if (kMean) {
+                w[0] += bf16_lo(v[u][0]);
+                w[1] += bf16_hi(v[u][0]);
+                w[2] += bf16_lo(v[u][1]);
+                w[3] += bf16_hi(v[u][1]);
+            } else {
+                const bool neg = e0 < kHeadDim;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float x0 = bf16_lo(v[u][j]), x1 = bf16_hi(v[u][j]);
+                    w[2 * j] += neg ? fminf(x0, 0.f) : fmaxf(x0, 0.f);
+                    w[2 * j + 1] += neg ? fminf(x1, 0.f) : fmaxf(x1, 0.f);
+                }
+            }
+        }
+    };
+    add_rows(0);  // straight-line code: these loads go right behind the batch
+    for (int g0 = 8; g0 < G; g0 += 8)
+        add_rows(g0);
     for (int j0 = 0; j0 < my_pages; j0 += kScoreBatch) {
         u32x4_t cur[kScoreBatch];
 #pragma unroll

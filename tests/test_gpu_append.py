@@ -130,6 +130,17 @@ def test_fused_random_shapes(seed):
     fused_check(G, Hkv, ps, tuple(lengths), 5100 + seed, sched, skip_last=seed % 2 == 0)
 
 
+@pytest.mark.parametrize("G,n_bins", [(16, 256), (12, 300)])
+def test_fused_large_groups_and_many_bins(G, n_bins):
+    # more than 8 query heads per KV head (a second batch of query rows in the scoring
+    # prologue) and schedule tables staged in LDS (256 bins) or read from memory (300)
+    rng = np.random.default_rng(77 + n_bins)
+    sched = W.Schedule(16, tuple(int(x) for x in rng.integers(0, 7, n_bins)),
+                       tuple(int(x) for x in rng.integers(1, 10, n_bins)), 20)
+    log(f"case fused G={G} with {n_bins} schedule bins")
+    fused_check(G, 2, 16, (3000, 4097, 6000, 5), 90 + G, sched)
+
+
 def fused_check(G, Hkv, ps, lengths, seed, schedule, skip_last=True):
     """The fused append + selection equals the append followed by the selection bit for
     bit, and both match the oracle through attention."""

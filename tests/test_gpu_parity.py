@@ -129,6 +129,22 @@ def test_budget_edges(k_pages):
             assert r["gpu"]["k"][b] == nb
 
 
+def many_bins(n_bins, seed):
+    """A seeded schedule table of n_bins 16-token bins (fractions 1..9 / 20, floors 0..6)."""
+    rng = np.random.default_rng(seed)
+    return W.Schedule(16, tuple(int(x) for x in rng.integers(0, 7, n_bins)),
+                      tuple(int(x) for x in rng.integers(1, 10, n_bins)), 20)
+
+
+@pytest.mark.parametrize("n_bins", [256, 300])
+def test_schedule_tables_of_many_bins(n_bins):
+    # 256 bins: the scoring kernel stages the tables in LDS; more: it reads them from memory
+    log(f"case schedule of {n_bins} bins")
+    lengths = (4000, 17, 4096, 4097, 6000, 1)  # several bins, the last bin and past it
+    inp = small_inputs(3, 2, 16, lengths, seed=41, schedule=many_bins(n_bins, 5))
+    full_check(inp)
+
+
 def test_k_max_caps_the_budget():
     log("case k_max cap")
     inp = small_inputs(2, 2, 16, (3000, 5000), seed=8, schedule=W.fraction_budget(1, 2))
