@@ -47,10 +47,10 @@ __device__ __forceinline__ void slice_minmax(const uint16_t *__restrict__ src, i
         if (t0 >= valid)
             break;
         u32x4_t v[16];
-        v[0] = ld16(src + (size_t)t0 * kHeadDim);
+        v[0] = ld16_nt(src + (size_t)t0 * kHeadDim);
 #pragma unroll
         for (int t = 1; t < 16; ++t)
-            v[t] = (t0 + t < valid) ? ld16(src + (size_t)(t0 + t) * kHeadDim) : v[0];
+            v[t] = (t0 + t < valid) ? ld16_nt(src + (size_t)(t0 + t) * kHeadDim) : v[0];
         // token t0 is valid; re-folding it for slots past the length changes nothing.
 #pragma unroll
         for (int t = 0; t < 16; ++t)
@@ -82,7 +82,7 @@ __device__ __forceinline__ void slice_sum(const uint16_t *__restrict__ src, int 
         u32x4_t v[16];
 #pragma unroll
         for (int t = 0; t < 16; ++t)
-            v[t] = (t < nt) ? ld16(src + (size_t)(t0 + t) * kHeadDim) : (u32x4_t){0u, 0u, 0u, 0u};
+            v[t] = (t < nt) ? ld16_nt(src + (size_t)(t0 + t) * kHeadDim) : (u32x4_t){0u, 0u, 0u, 0u};
 #pragma unroll
         for (int t = 0; t < 16; ++t) {
             if (t < nt) {
