@@ -51,8 +51,9 @@
  *                                  being decoded (0 allowed)
  *      idx          int32 [batch][num_kv_heads][k_max]  selected logical pages
  *      out          fp32 or bf16 [batch][num_q_heads][head_dim]
- *    Sequence b uses logical pages 0 .. ceil(seq_lens[b] / page_size) - 1;
- *    only those block-table entries are read.  Query head j reads KV head
+ *    Sequence b uses logical pages 0 .. ceil(seq_lens[b] / page_size) - 1; the
+ *    rest of its block-table row may be read (the array must be whole) but its
+ *    values never matter.  Query head j reads KV head
  *    j / G with G = num_q_heads / num_kv_heads (grouped-query attention).
  *  - Supported shapes: head_dim == 128; page_size in {16, 32, 64, 128};
  *    landmark in {SPARROW_LANDMARK_MINMAX, SPARROW_LANDMARK_MEAN};
