@@ -201,3 +201,42 @@ def test_mean_landmark_with_absent_pages():
     ora_idx = oracle.select(lens, ora_k, s32, PS, k_max)
     check_indices(k.cpu().numpy(), idx.cpu().numpy(), ora_k, ora_idx, s32, s64, lens, PS,
                   k_max)
+
+
+def test_block_table_entries_past_the_sequence_do_not_matter():
+    # the entries past a sequence's last page may be read but never used: garbage there
+    # (negative, past the cache, or another sequence's pages) leaves every output unchanged
+    log("case garbage past each sequence's pages")
+    w = W.small(B=len(LENGTHS), Hq=G * HKV, Hkv=HKV, ps=PS, lengths=LENGTHS, seed=23,
+                schedule=W.fraction_budget(1, 3))
+    inp = W.generate(w, DEV, lengths=list(LENGTHS))
+    s = inp.workload.schedule
+    k_max = S.budget_bound(inp.lens_host, PS, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den)
+    kn = torch.ones((len(LENGTHS), HKV, 128), device=DEV).to(torch.bfloat16)
+
+    def run(bt):
+        kc, vc = inp.k_cache.clone(), inp.v_cache.clone()
+        meta = S.new_meta(inp.num_phys_pages, HKV, DEV)
+        S.page_meta_update(kc, bt, inp.seq_lens, meta)
+        step = S.SparseDecodeStep(inp.q, kc, vc, bt, inp.seq_lens, meta, inp.min_pages,
+                                  inp.frac_num, s.frac_den, s.bin_tokens, k_max)
+        sp = torch.cuda.current_stream().cuda_stream
+        step.append_score_topk(kn, kn, sp)
+        step.attend(sp)
+        dense = S.dense_decode_attn(inp.q, kc, vc, bt, inp.seq_lens, SCALE)
+        torch.cuda.synchronize()
+        return [x.cpu() for x in (meta.view(torch.int16), kc.view(torch.int16), step.k,
+                                  step.idx, step.out, dense)]
+
+    ref = run(inp.block_table)
+    bt = inp.block_table.cpu().numpy().copy()
+    rng = np.random.default_rng(3)
+    P = inp.num_phys_pages
+    for b, L in enumerate(LENGTHS):
+        n = (L + PS - 1) // PS
+        tail = bt.shape[1] - n
+        bt[b, n:] = rng.choice([-1, -(2**31), P, 2**31 - 1, 0, 1, P - 1], size=tail)
+    got = run(torch.as_tensor(bt, device=DEV))
+    for x, y in zip(got, ref):
+        assert torch.equal(x, y)
