@@ -129,6 +129,15 @@ def test_budget_edges(k_pages):
             assert r["gpu"]["k"][b] == nb
 
 
+def test_every_sequence_within_one_page():
+    # a one-column block table: one scoring block, one page per unit, budgets of 0 or 1
+    log("case one page per sequence")
+    inp = small_inputs(4, 2, 16, (1, 16, 7, 0, 12), seed=43, schedule=W.fixed_budget(1),
+                       extra_pages=0)
+    assert inp.max_pages == 1
+    full_check(inp)
+
+
 def many_bins(n_bins, seed):
     """A seeded schedule table of n_bins 16-token bins (fractions 1..9 / 20, floors 0..6)."""
     rng = np.random.default_rng(seed)
