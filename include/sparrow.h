@@ -285,7 +285,9 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
  *     p = softmax(inv_temperature * a),  q = softmax(inv_temperature * b),
  *     alpha[t] = sum_x min(p(x), q(x))
  * computed in fp32 (two passes: log-sum-exp of both rows, then the sum).  Agrees
- * with an fp64 evaluation to about 1e-5.  logits_dtype is SPARROW_LOGITS_F32 or
+ * with an fp64 evaluation to about 1e-5.  A logit of -inf (a masked vocabulary entry)
+ * has probability 0; each row needs at least one finite logit, and -inf entries need
+ * inv_temperature > 0.  NaN and +inf logits are not supported.  logits_dtype is SPARROW_LOGITS_F32 or
  * SPARROW_LOGITS_BF16; rows are contiguous ([num_tokens][vocab], row-major).
  *
  * Arguments: num_tokens >= 0; vocab >= 1; target_logits, draft_logits (device,
@@ -333,6 +335,41 @@ int sparrow_acceptance_rate_topk(int64_t num_tokens, int32_t k, const float *lp_
 int sparrow_tail_stats(int64_t num_tokens, const float *alpha, const int32_t *positions,
                        int32_t bin_tokens, int32_t n_bins, double percentile, double *quantile,
                        double *mean, int64_t *count, void *stream);
+
+/*
+ * Read-only streaming reference (a measurement helper, not a step of the method): reads
+ * `bytes` bytes at src once, with the 16-byte non-temporal vector loads and the
+ * consecutive-lanes layout of the decode-step kernels, from a grid that keeps every
+ * compute unit busy, and adds every 32-bit word of the buffer into *checksum (modulo
+ * 2^32, on top of its current value: the caller sets it, usually to 0).  Timing a call
+ * gives the rate a pure read stream sustains on the device, the practical ceiling of the
+ * read-dominated decode kernels beside the HBM peak.
+ *
+ * Arguments: src (device, 16-byte aligned, may be NULL when bytes is 0); bytes >= 0, a
+ * multiple of 16; checksum (device uint32, 4-byte aligned); stream.
+ * Errors: SPARROW_EINVAL (null or misaligned pointer, bad size), SPARROW_EHIP.
+ */
+int sparrow_stream_read(const void *src, int64_t bytes, uint32_t *checksum, void *stream);
+
+/*
+ * Host-side page budgets of the dynamic sparsity schedule (Sec. 3.2 Method box; the
+ * formula of sparrow_schedule_t, evaluated by the same code the scoring kernels use), to
+ * size k_max before a call of sparrow_page_score_topk or sparrow_append_score_topk.
+ *
+ * For every b < num_seqs: budgets[b] = k_b of a sequence of seq_lens[b] tokens (0 when
+ * seq_lens[b] <= 0), not capped by any k_max.  Returns max(1, max_b k_b), the smallest
+ * k_max that caps no budget, or a negative status.
+ *
+ * Arguments: seq_lens (HOST int32 [num_seqs], may be NULL when num_seqs is 0); num_seqs
+ * >= 0; page_size >= 1; bin_tokens >= 1; n_bins >= 1; min_pages, frac_num (HOST int32
+ * [n_bins], non-negative); frac_den >= 1; budgets (HOST int32 [num_seqs], written) or
+ * NULL.  Every pointer is a host pointer; nothing runs on the GPU.
+ * Errors: SPARROW_EINVAL (bad size, null table, negative table entry, or a length above
+ * page_size * SPARROW_MAX_PAGES_PER_SEQ).
+ */
+int32_t sparrow_budget_bound(const int32_t *seq_lens, int64_t num_seqs, int32_t page_size,
+                             int32_t bin_tokens, int32_t n_bins, const int32_t *min_pages,
+                             const int32_t *frac_num, int32_t frac_den, int32_t *budgets);
 
 /*
  * Workspace bytes needed by one call of `op` (SPARROW_OP_*) with this shape

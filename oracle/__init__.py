@@ -66,6 +66,8 @@ def _load():
     lib.oracle_page_scores_mean.restype = None
     lib.oracle_select_forced.argtypes = [_i32, _i32, _i32, _i32, _p, _p, _p, _i32, _i32, _i32, _p]
     lib.oracle_select_forced.restype = None
+    lib.oracle_set_num_threads.argtypes = [_i32]
+    lib.oracle_set_num_threads.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = _i32
     _lib = lib
@@ -80,6 +82,11 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (default: every host core)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def budget(L, ps, bin_tokens, min_pages, frac_num, frac_den) -> int:
@@ -156,8 +163,9 @@ def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta, inpla
     return kc, vc, mt
 
 
-def page_scores(q, meta, block_table, seq_lens, ps):
-    """(scores32, scores64), each ``[B][Hkv][max_pages]``; entries past ``n_b`` are NaN."""
+def page_scores(q, meta, block_table, seq_lens, ps, fp64=True):
+    """(scores32, scores64), each ``[B][Hkv][max_pages]``; entries past ``n_b`` are NaN.
+    ``fp64=False`` skips the fp64 adjudication copy (scores64 is then None)."""
     B, Hq, D = q.shape
     P, Hkv, _, _ = meta.shape
     max_pages = block_table.shape[1]
@@ -166,9 +174,9 @@ def page_scores(q, meta, block_table, seq_lens, ps):
     bt, btp = _c(block_table, np.int32)
     sl, slp = _c(seq_lens, np.int32)
     s32 = np.full((B, Hkv, max_pages), np.nan, np.float32)
-    s64 = np.full((B, Hkv, max_pages), np.nan, np.float64)
+    s64 = np.full((B, Hkv, max_pages), np.nan, np.float64) if fp64 else None
     _load().oracle_page_scores(B, Hq, Hkv, D, ps, max_pages, qp, mp, btp, slp,
-                               s32.ctypes.data, s64.ctypes.data)
+                               s32.ctypes.data, None if s64 is None else s64.ctypes.data)
     return s32, s64
 
 
@@ -301,8 +309,9 @@ def page_key_sums(k_cache, block_table, seq_lens, first_pos=None, sums=None, inp
     return out
 
 
-def page_scores_mean(q, sums, block_table, seq_lens, ps):
-    """Mean-landmark page scores (scores32, scores64), each ``[B][Hkv][max_pages]``."""
+def page_scores_mean(q, sums, block_table, seq_lens, ps, fp64=True):
+    """Mean-landmark page scores (scores32, scores64), each ``[B][Hkv][max_pages]``;
+    ``fp64=False`` skips the fp64 copy (scores64 is then None)."""
     B, Hq, D = q.shape
     P, Hkv, _ = sums.shape
     max_pages = block_table.shape[1]
@@ -311,9 +320,9 @@ def page_scores_mean(q, sums, block_table, seq_lens, ps):
     bt, btp = _c(block_table, np.int32)
     sl, slp = _c(seq_lens, np.int32)
     s32 = np.full((B, Hkv, max_pages), np.nan, np.float32)
-    s64 = np.full((B, Hkv, max_pages), np.nan, np.float64)
+    s64 = np.full((B, Hkv, max_pages), np.nan, np.float64) if fp64 else None
     _load().oracle_page_scores_mean(B, Hq, Hkv, D, ps, max_pages, qp, sp_, btp, slp,
-                                    s32.ctypes.data, s64.ctypes.data)
+                                    s32.ctypes.data, None if s64 is None else s64.ctypes.data)
     return s32, s64
 
 

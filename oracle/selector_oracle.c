@@ -92,7 +92,8 @@ void oracle_page_scores_mean(int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int3
                     double s64 = 0.0;
                     for (int32_t i = 0; i < D; ++i) {
                         s32 += bf16f(qj[i]) * (sm[i] / (float)valid);
-                        s64 += (double)bf16f(qj[i]) * ((double)sm[i] / (double)valid);
+                        if (scores64) /* the adjudication copy, only when asked for */
+                            s64 += (double)bf16f(qj[i]) * ((double)sm[i] / (double)valid);
                     }
                     tot32 += s32;
                     tot64 += s64;

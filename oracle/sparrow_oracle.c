@@ -227,9 +227,11 @@ void oracle_page_scores(int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int32_t p
                         float lo = qi * bf16_value_f(mn[i]); /* exact: bf16 x bf16 */
                         float hi = qi * bf16_value_f(mx[i]);
                         s32 += lo > hi ? lo : hi;
-                        double lo64 = (double)qi * bf16_value(mn[i]);
-                        double hi64 = (double)qi * bf16_value(mx[i]);
-                        s64 += lo64 > hi64 ? lo64 : hi64;
+                        if (scores64) { /* the adjudication copy, only when asked for */
+                            double lo64 = (double)qi * bf16_value(mn[i]);
+                            double hi64 = (double)qi * bf16_value(mx[i]);
+                            s64 += lo64 > hi64 ? lo64 : hi64;
+                        }
                     }
                     head_sum32 += s32;
                     head_sum64 += s64;
@@ -401,6 +403,17 @@ double oracle_weight_sum(int32_t D, int64_t n_tok, const uint16_t *qj, const uin
         total += exp(z[t] - m) / denom;
     free(z);
     return total;
+}
+
+/* Threads of the parallel loops (the OpenMP default is every host core). */
+void oracle_set_num_threads(int32_t n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n < 1 ? 1 : n);
+#else
+    (void)n;
+#endif
 }
 
 int32_t oracle_num_threads(void)

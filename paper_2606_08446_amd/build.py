@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsparrow.so")
 SOURCES = ["api.hip", "meta.hip", "append.hip", "score_topk.hip", "attention.hip",
-           "acceptance.hip"]
+           "acceptance.hip", "measure.hip"]
 ARCH = "gfx950"
 # Packed fp32 VALU ops are switched off for every device compile.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

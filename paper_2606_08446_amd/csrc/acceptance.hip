@@ -82,10 +82,13 @@ __device__ __forceinline__ void lse_add(Lse &r, const float (&x)[N])
         r.s = r.m == -INFINITY ? 0.f : r.s * __expf(r.m - mx);
         r.m = mx;
     }
+    // While every entry seen is -inf (masked vocabulary entries), the chunk adds nothing:
+    // exp(x - 0) = 0 for x = -inf, where x - r.m would be -inf - (-inf) = NaN.
+    const float m = r.m == -INFINITY ? 0.f : r.m;
     float s = 0.f;
 #pragma unroll
     for (int e = 0; e < N; ++e)
-        s += __expf(x[e] - r.m);
+        s += __expf(x[e] - m);
     r.s += s;
 }
 

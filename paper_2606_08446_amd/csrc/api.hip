@@ -256,6 +256,47 @@ int sparrow_tail_stats(int64_t num_tokens, const float *alpha, const int32_t *po
                                        static_cast<hipStream_t>(stream)));
 }
 
+int sparrow_stream_read(const void *src, int64_t bytes, uint32_t *checksum, void *stream)
+{
+    if (bytes < 0 || (bytes & 15) != 0 || !checksum || (bytes > 0 && !src))
+        return SPARROW_EINVAL;
+    if (!al16(src) || !al4(checksum))
+        return SPARROW_EINVAL;
+    if (bytes == 0)
+        return SPARROW_OK;
+    return status_of(launch_stream_read(src, bytes, checksum, static_cast<hipStream_t>(stream)));
+}
+
+int32_t sparrow_budget_bound(const int32_t *seq_lens, int64_t num_seqs, int32_t page_size,
+                             int32_t bin_tokens, int32_t n_bins, const int32_t *min_pages,
+                             const int32_t *frac_num, int32_t frac_den, int32_t *budgets)
+{
+    if (num_seqs < 0 || page_size < 1 || bin_tokens < 1 || n_bins < 1 || frac_den < 1)
+        return SPARROW_EINVAL;
+    if (!min_pages || !frac_num || (num_seqs > 0 && !seq_lens))
+        return SPARROW_EINVAL;
+    for (int32_t i = 0; i < n_bins; ++i)
+        if (min_pages[i] < 0 || frac_num[i] < 0)
+            return SPARROW_EINVAL;
+    const int64_t max_len = (int64_t)page_size * SPARROW_MAX_PAGES_PER_SEQ;
+    int32_t best = 1;
+    for (int64_t b = 0; b < num_seqs; ++b) {
+        const int32_t L = seq_lens[b];
+        if (L > max_len)
+            return SPARROW_EINVAL;
+        int32_t k = 0;
+        if (L > 0) {
+            const int bin = budget_bin(L, bin_tokens, n_bins);
+            k = budget_from(L, page_size, min_pages[bin], frac_num[bin], frac_den, 0x7fffffff);
+        }
+        if (budgets)
+            budgets[b] = k;
+        if (k > best)
+            best = k;
+    }
+    return best;
+}
+
 size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32_t op)
 {
     if (check_shape(shape) != SPARROW_OK)

@@ -118,18 +118,26 @@ __device__ __forceinline__ int clamp_len(int L, int ps, int max_pages)
     return L < 0 ? 0 : (L > cap ? cap : L);
 }
 
-// Schedule bin of a sequence of L >= 1 tokens (the position of its last token).
-__device__ __forceinline__ int budget_bin(int L, const Sched &s)
+// Schedule bin of a sequence of L >= 1 tokens (the position of its last token).  Shared by
+// the kernels and the host-side bound (sparrow_budget_bound), so both use one definition.
+__host__ __device__ __forceinline__ int budget_bin(int L, int bin_tokens, int n_bins)
 {
-    const int bin = (L - 1) / s.bin_tokens;
-    return bin > s.n_bins - 1 ? s.n_bins - 1 : bin;
+    const int bin = (L - 1) / bin_tokens;
+    return bin > n_bins - 1 ? n_bins - 1 : bin;
 }
 
-// Page budget of a sequence of L >= 1 tokens from its bin's table entries, capped at k_max.
-__device__ __forceinline__ int budget_from(int L, int ps, int32_t min_pages, int32_t frac_num,
-                                           int32_t frac_den, int k_max)
+__device__ __forceinline__ int budget_bin(int L, const Sched &s)
 {
-    const int64_t n = (L + ps - 1) / ps;
+    return budget_bin(L, s.bin_tokens, s.n_bins);
+}
+
+// Page budget of a sequence of L >= 1 tokens from its bin's table entries, capped at k_max:
+// clamp(max(min_pages, ceil(n * frac_num / frac_den)), 1, n) with n = ceil(L / ps).
+__host__ __device__ __forceinline__ int budget_from(int L, int ps, int32_t min_pages,
+                                                    int32_t frac_num, int32_t frac_den,
+                                                    int k_max)
+{
+    const int64_t n = ((int64_t)L + ps - 1) / ps;
     int64_t k = (n * (int64_t)frac_num + frac_den - 1) / frac_den;
     if (k < min_pages)
         k = min_pages;
@@ -184,6 +192,9 @@ hipError_t launch_acceptance_topk(int64_t T, int K, const float *lp_target, cons
 hipError_t launch_tail_stats(int64_t T, const float *alpha, const int32_t *pos, int bin_tokens,
                              int n_bins, double pct, double *quantile, double *mean,
                              int64_t *count, hipStream_t stream);
+
+hipError_t launch_stream_read(const void *src, int64_t bytes, uint32_t *checksum,
+                              hipStream_t stream);
 
 struct AttnPlan {
     size_t plan_bytes;       // page offsets and unit wave ranges at the start of the workspace

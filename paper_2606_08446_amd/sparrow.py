@@ -41,7 +41,8 @@ SPARROW_OP_DENSE_ATTN = 2
 EXPORTS = ("sparrow_page_meta_update", "sparrow_append_kv", "sparrow_page_score_topk",
            "sparrow_append_score_topk", "sparrow_sparse_decode_attn", "sparrow_dense_decode_attn",
            "sparrow_acceptance_rate", "sparrow_acceptance_rate_topk", "sparrow_tail_stats",
-           "sparrow_workspace_size", "sparrow_status_string")
+           "sparrow_stream_read", "sparrow_budget_bound", "sparrow_workspace_size",
+           "sparrow_status_string")
 
 
 class SparrowError(RuntimeError):
@@ -95,8 +96,11 @@ def load():
     lib.sparrow_acceptance_rate_topk.argtypes = [ctypes.c_int64, _i32, _p, _p, _p, _p]
     lib.sparrow_tail_stats.argtypes = [ctypes.c_int64, _p, _p, _i32, _i32, ctypes.c_double, _p,
                                        _p, _p, _p]
-    for fn in EXPORTS[:9]:
+    lib.sparrow_stream_read.argtypes = [_p, ctypes.c_int64, _p, _p]
+    for fn in EXPORTS[:10]:
         getattr(lib, fn).restype = ctypes.c_int
+    lib.sparrow_budget_bound.argtypes = [_p, ctypes.c_int64, _i32, _i32, _i32, _p, _p, _i32, _p]
+    lib.sparrow_budget_bound.restype = ctypes.c_int32
     lib.sparrow_workspace_size.argtypes = [sp, _i32, _i32]
     lib.sparrow_workspace_size.restype = ctypes.c_size_t
     lib.sparrow_status_string.argtypes = [_i32]
@@ -162,6 +166,16 @@ def sparrow_tail_stats(num_tokens, alpha, positions, bin_tokens, n_bins, percent
                                      quantile, mean, count, stream)
 
 
+def sparrow_stream_read(src, nbytes, checksum, stream):
+    return load().sparrow_stream_read(src, nbytes, checksum, stream)
+
+
+def sparrow_budget_bound(seq_lens, num_seqs, page_size, bin_tokens, n_bins, min_pages, frac_num,
+                         frac_den, budgets) -> int:
+    return int(load().sparrow_budget_bound(seq_lens, num_seqs, page_size, bin_tokens, n_bins,
+                                           min_pages, frac_num, frac_den, budgets))
+
+
 def sparrow_workspace_size(shape, k_max, op) -> int:
     return int(load().sparrow_workspace_size(ctypes.byref(shape), k_max, op))
 
@@ -197,20 +211,28 @@ def new_meta(num_phys_pages, num_kv_heads, device, landmark=SPARROW_LANDMARK_MIN
                        device=device)
 
 
+def _host_i32(values) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(values, dtype=np.int64).astype(np.int32))
+
+
+def budgets(seq_lens: Sequence[int], page_size: int, bin_tokens: int, min_pages: Sequence[int],
+            frac_num: Sequence[int], frac_den: int):
+    """(per-sequence schedule budgets int32 [B], their bound) from host-known lengths, computed
+    by the library's sparrow_budget_bound (host code, no GPU needed)."""
+    lens = _host_i32(seq_lens)
+    mp, fn = _host_i32(min_pages), _host_i32(frac_num)
+    out = np.zeros(len(lens), dtype=np.int32)
+    rc = sparrow_budget_bound(lens.ctypes.data, len(lens), int(page_size), int(bin_tokens),
+                              len(mp), mp.ctypes.data, fn.ctypes.data, int(frac_den),
+                              out.ctypes.data)
+    _check("sparrow_budget_bound", min(rc, 0))
+    return out, rc
+
+
 def budget_bound(seq_lens: Sequence[int], page_size: int, bin_tokens: int,
                  min_pages: Sequence[int], frac_num: Sequence[int], frac_den: int) -> int:
-    """Largest schedule budget over host-known lengths, to size ``k_max`` (at least 1)."""
-    best = 1
-    nb = len(min_pages)
-    for L in seq_lens:
-        L = int(L)
-        if L <= 0:
-            continue
-        n = -(-L // page_size)
-        b = min((L - 1) // bin_tokens, nb - 1)
-        k = max(int(min_pages[b]), -(-(n * int(frac_num[b])) // frac_den))
-        best = max(best, min(max(k, 1), n))
-    return best
+    """Largest schedule budget over host-known lengths (at least 1), to size ``k_max``."""
+    return budgets(seq_lens, page_size, bin_tokens, min_pages, frac_num, frac_den)[1]
 
 
 def _ptr(t) -> Optional[int]:
@@ -379,6 +401,19 @@ def tail_stats(alpha, positions, bin_tokens, n_bins, percentile=5.0):
         alpha.numel(), _ptr(alpha), _ptr(positions), int(bin_tokens), int(n_bins),
         float(percentile), _ptr(q), _ptr(m), _ptr(c), _stream(dev)))
     return q, m, c
+
+
+def stream_read(buf, checksum=None):
+    """Read a device buffer once through the library's streaming reference; returns the
+    uint32 checksum tensor (sum of the buffer's 32-bit words modulo 2^32, added to
+    ``checksum`` when given, else to a new zero)."""
+    import torch
+    _require_device(buf)
+    if checksum is None:
+        checksum = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    _check("sparrow_stream_read", sparrow_stream_read(
+        _ptr(buf), buf.numel() * buf.element_size(), _ptr(checksum), _stream(buf.device)))
+    return checksum
 
 
 class SparseDecodeStep:

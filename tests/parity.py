@@ -67,6 +67,18 @@ def check_meta(gpu_meta, ora_meta, bt, lens, ps):
         np.testing.assert_array_equal(gpu_meta[pages], ora_meta[pages])
 
 
+def oracle_budgets(lens, ps, bin_tokens, min_pages, frac_num, frac_den, k_max,
+                   capped=False):
+    """The oracle's schedule budgets, uncapped.  Unless a test caps k_max on purpose
+    (capped=True), k_max must cover every budget: a k_max sized below the schedule would
+    truncate the budgets on both sides alike and hide the error."""
+    k = oracle.budgets(lens, ps, bin_tokens, min_pages, frac_num, frac_den)
+    if capped:
+        return np.minimum(k, k_max).astype(np.int32)
+    assert int(np.max(k, initial=0)) <= k_max, ("k_max below a schedule budget", k_max)
+    return k.astype(np.int32)
+
+
 def rank_boundary(s32_row, s64_row, n, k):
     """fp64 score of the oracle's k-th page (ranking by fp32 score, ties to lower index)."""
     order = sorted(range(n), key=lambda p: (-float(s32_row[p]), p))
@@ -109,8 +121,10 @@ def check_out(gpu, ref, what):
     assert mx <= MAX_ABS and mean <= MEAN_ABS, (what, mx, mean)
 
 
-def full_check(inp: W.Inputs, k_max=None, dense=True, out_dtype=S.SPARROW_OUT_F32):
-    """Whole sparse step plus dense on the GPU vs the oracle, every sequence."""
+def full_check(inp: W.Inputs, k_max=None, dense=True, out_dtype=S.SPARROW_OUT_F32,
+               capped=False):
+    """Whole sparse step plus dense on the GPU vs the oracle, every sequence.  ``capped``: the
+    test passes a k_max below some budgets on purpose."""
     w = inp.workload
     s = w.schedule
     ps = w.page_size
@@ -122,8 +136,8 @@ def full_check(inp: W.Inputs, k_max=None, dense=True, out_dtype=S.SPARROW_OUT_F3
     ora_meta = oracle.page_meta(h["k"], h["bt"], h["lens"])
     check_meta(g["meta"], ora_meta, h["bt"], h["lens"], ps)
     s32, s64 = oracle.page_scores(h["q"], ora_meta, h["bt"], h["lens"], ps)
-    ora_k = np.minimum(oracle.budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max, capped=capped)
     ora_idx = oracle.select(h["lens"], ora_k, s32, ps, k_max)
     excused = check_indices(g["k"], g["idx"], ora_k, ora_idx, s32, s64, h["lens"], ps, k_max)
     # attention over the GPU's (validated) page lists

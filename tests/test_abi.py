@@ -210,16 +210,71 @@ def test_status_strings(lib):
     assert S.sparrow_status_string(-3) != S.sparrow_status_string(-1)
 
 
-@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c5"])
-def test_host_budget_bound_matches_oracle(cfg):
-    w = W.CONFIGS[cfg]
+def schedule_workloads():
+    """Every schedule a workload uses: C1-C5, C4's five fractions, the Table 4 study."""
+    ws = [W.CONFIGS[c] for c in ("c1", "c2", "c3", "c4", "c5")]
+    ws += [W.c4_with_fraction(i) for i in range(len(W.C4_FRACTIONS))]
+    ws += [W.table4(ps, 16384) for ps in (16, 32, 64, 128)]
+    return ws
+
+
+@pytest.mark.parametrize("w", schedule_workloads(), ids=lambda w: w.name)
+def test_host_budget_bound_matches_oracle(w):
+    # sparrow_budget_bound (the library's schedule arithmetic, run on the host) against the
+    # oracle's budgets, per sequence, on lengths over and around the workload's range
     s = w.schedule
     rng = np.random.default_rng(3)
-    lens = rng.integers(w.len_lo, w.len_hi + 1, size=200)
-    want = int(oracle.budgets(lens, w.page_size, s.bin_tokens, s.min_pages, s.frac_num,
-                              s.frac_den).max())
+    lens = np.concatenate([rng.integers(w.len_lo, w.len_hi + 1, size=300),
+                           [0, 1, w.page_size, w.page_size + 1, w.len_lo, w.len_hi,
+                            w.len_hi + 5000, 2048, 2049]])
+    want = oracle.budgets(lens, w.page_size, s.bin_tokens, s.min_pages, s.frac_num, s.frac_den)
+    got, bound = S.budgets(lens, w.page_size, s.bin_tokens, s.min_pages, s.frac_num, s.frac_den)
+    np.testing.assert_array_equal(got, want)
+    assert bound == max(1, int(want.max()))
     assert S.budget_bound(lens, w.page_size, s.bin_tokens, s.min_pages, s.frac_num,
-                          s.frac_den) == want
+                          s.frac_den) == bound
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_host_budget_bound_random_schedules(seed):
+    rng = np.random.default_rng(500 + seed)
+    nb = int(rng.integers(1, 300))
+    sch = W.Schedule(int(rng.choice([1, 7, 256, 2048])),
+                     tuple(int(x) for x in rng.integers(0, 50, size=nb)),
+                     tuple(int(x) for x in rng.integers(0, 1200, size=nb)),
+                     int(rng.choice([1, 3, 1000])))
+    ps = int(rng.choice([16, 32, 64, 128]))
+    lens = rng.integers(-3, 60000, size=400)
+    want = oracle.budgets(np.maximum(lens, 0), ps, sch.bin_tokens, sch.min_pages, sch.frac_num,
+                          sch.frac_den)
+    got, bound = S.budgets(lens, ps, sch.bin_tokens, sch.min_pages, sch.frac_num, sch.frac_den)
+    np.testing.assert_array_equal(got, want)
+    assert bound == max(1, int(want.max()))
+
+
+def test_host_budget_bound_validates_arguments(lib):
+    lens = np.array([100, 200], np.int32)
+    mp = np.array([4], np.int32)
+    fn = np.array([1], np.int32)
+
+    def call(lens_p=lens.ctypes.data, n=2, ps=16, bt=2048, nb=1, mp_p=mp.ctypes.data,
+             fn_p=fn.ctypes.data, den=10, out=None):
+        return S.sparrow_budget_bound(lens_p, n, ps, bt, nb, mp_p, fn_p, den, out)
+    assert call() == 4                       # ceil(13 / 10) = 2 < floor 4
+    assert call(n=0, lens_p=None) == 1
+    assert call(lens_p=None) == S.SPARROW_EINVAL
+    assert call(n=-1) == S.SPARROW_EINVAL
+    for kw in (dict(ps=0), dict(bt=0), dict(nb=0), dict(den=0), dict(mp_p=None),
+               dict(fn_p=None)):
+        assert call(**kw) == S.SPARROW_EINVAL, kw
+    neg = np.array([-1], np.int32)
+    assert call(mp_p=neg.ctypes.data) == S.SPARROW_EINVAL
+    assert call(fn_p=neg.ctypes.data) == S.SPARROW_EINVAL
+    too_long = np.array([16 * S.SPARROW_MAX_PAGES_PER_SEQ + 1], np.int32)
+    assert call(lens_p=too_long.ctypes.data, n=1) == S.SPARROW_EINVAL
+    longest = np.array([16 * S.SPARROW_MAX_PAGES_PER_SEQ], np.int32)
+    assert call(lens_p=longest.ctypes.data, n=1, fn_p=np.array([10], np.int32).ctypes.data) == \
+        S.SPARROW_MAX_PAGES_PER_SEQ
 
 
 def test_tensor_wrappers_refuse_host_tensors():
@@ -287,3 +342,14 @@ def test_acceptance_entry_points_validate_arguments(lib):
         assert tail(**{arg: None}) == S.SPARROW_EINVAL
     assert tail(n=0, q=None) == S.SPARROW_EINVAL
     assert tail(q=FAKE + 4) == S.SPARROW_EINVAL               # fp64 outputs need 8-byte alignment
+
+
+def test_stream_read_validates_arguments(lib):
+    assert S.sparrow_stream_read(FAKE, 0, FAKE, None) == S.SPARROW_OK
+    assert S.sparrow_stream_read(None, 0, FAKE, None) == S.SPARROW_OK
+    assert S.sparrow_stream_read(None, 16, FAKE, None) == S.SPARROW_EINVAL
+    assert S.sparrow_stream_read(FAKE, 16, None, None) == S.SPARROW_EINVAL
+    assert S.sparrow_stream_read(FAKE, -16, FAKE, None) == S.SPARROW_EINVAL
+    assert S.sparrow_stream_read(FAKE, 24, FAKE, None) == S.SPARROW_EINVAL   # not a multiple of 16
+    assert S.sparrow_stream_read(FAKE + 8, 16, FAKE, None) == S.SPARROW_EINVAL
+    assert S.sparrow_stream_read(FAKE, 16, FAKE + 2, None) == S.SPARROW_EINVAL

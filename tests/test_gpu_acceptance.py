@@ -72,6 +72,44 @@ def test_acceptance_random_shapes(seed):
     assert err.max() <= ALPHA_TOL
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("off", [0, 1])
+def test_acceptance_masked_entries(dtype, off):
+    # runs of -inf logits (masked vocabulary entries) where every thread's first vector is
+    # masked (the first 1024 16-byte vectors), in the scalar head and tail of unaligned rows,
+    # a row whose only finite entry is the last, and rows masked differently on the two
+    # sides (probability 0 under one distribution only)
+    log(f"case acceptance masked {dtype} offset={off}")
+    T, V = 6, 13001
+    li = W.generate_logits(W.small_logits(T=T + 1, V=V, seed=80, dtype=dtype), DEV)
+    t = li.target.view(-1)[off:off + T * V].view(T, V)   # a view: rows keep the offset
+    d = li.draft.view(-1)[off:off + T * V].view(T, V)
+    per_vec = 4 if dtype == "f32" else 8
+    ninf = float("-inf")
+    t[0, :1024 * per_vec + 5] = ninf
+    d[0, :1024 * per_vec + 5] = ninf
+    t[1, :3] = ninf
+    d[1, :3] = ninf
+    t[1, -7:] = ninf
+    d[1, -7:] = ninf
+    t[2, :-1] = ninf
+    d[2, :-1] = ninf
+    t[3, 100:6000] = ninf
+    d[4, 2000:9000] = ninf
+    t[5, ::2] = ninf
+    d[5, ::2] = ninf
+    for tau in (1.0, 0.7):
+        got = S.acceptance_rate(t, d, tau)
+        torch.cuda.synchronize()
+        ref = oracle.acceptance(host_rows(t), host_rows(d), tau)
+        g = got.cpu().numpy().astype(np.float64)
+        assert np.isfinite(g).all(), g
+        err = np.abs(g - ref)
+        log(f"  tau={tau} max abs err {err.max():.2e}")
+        assert err.max() <= ALPHA_TOL
+        assert abs(g[2] - 1.0) <= 2e-6     # one finite entry in both rows: alpha = 1
+
+
 def test_acceptance_unaligned_row_starts():
     # views whose rows start off a 16-byte boundary (both rows in the same phase)
     li = W.generate_logits(W.small_logits(T=9, V=2051, seed=4), DEV)

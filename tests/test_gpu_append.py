@@ -10,7 +10,8 @@ import oracle
 from paper_2606_08446_amd import sparrow as S
 from paper_2606_08446_amd import workloads as W
 
-from parity import (SCALE, check_indices, check_out, host, log, sample_inputs)
+from parity import (SCALE, check_indices, check_out, host, log, oracle_budgets,
+                    sample_inputs)
 
 pytestmark = pytest.mark.gpu
 
@@ -169,8 +170,8 @@ def fused_check(G, Hkv, ps, lengths, seed, schedule, skip_last=True):
     np.testing.assert_array_equal(W.bf16_bits(meta_b), mt)
     lens_eff = np.minimum(h0["lens"], ps * inp.max_pages).astype(np.int32)
     s32, s64 = oracle.page_scores(h0["q"], mt, h0["bt"], lens_eff, ps)
-    ora_k = np.minimum(oracle.budgets(lens_eff, ps, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(lens_eff, ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(lens_eff, ora_k, s32, ps, k_max)
     check_indices(k_b.cpu().numpy(), idx_b.cpu().numpy(), ora_k, ora_idx, s32, s64, lens_eff,
                   ps, k_max)
@@ -257,8 +258,8 @@ def test_full_size_c5_fused_append_step():
         row = h["k"][h["bt"][i, pos // w.page_size], :, pos % w.page_size]
         np.testing.assert_array_equal(row, W.bf16_bits(kn[b]))
     s32, s64 = oracle.page_scores(h["q"], ora_meta, h["bt"], h["lens"], w.page_size)
-    ora_k = np.minimum(oracle.budgets(h["lens"], w.page_size, s.bin_tokens, s.min_pages,
-                                      s.frac_num, s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(h["lens"], w.page_size, s.bin_tokens, s.min_pages,
+                           s.frac_num, s.frac_den, k_max)
     ora_idx = oracle.select(h["lens"], ora_k, s32, w.page_size, k_max)
     check_indices(k.cpu().numpy()[seqs], idx.cpu().numpy()[seqs], ora_k, ora_idx, s32, s64,
                   h["lens"], w.page_size, k_max)

@@ -14,7 +14,7 @@ import oracle
 from paper_2606_08446_amd import sparrow as S
 from paper_2606_08446_amd import workloads as W
 
-from parity import SCALE, check_indices, check_out, host, log
+from parity import SCALE, check_indices, check_out, host, log, oracle_budgets
 
 pytestmark = pytest.mark.gpu
 
@@ -96,8 +96,8 @@ def test_block_table_entries_outside_the_cache():
                                inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, k_max)
     torch.cuda.synchronize()
     s32, s64 = oracle.page_scores(h["q"], ora_meta, btz, lens, PS)
-    ora_k = np.minimum(oracle.budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(lens, ora_k, s32, PS, k_max)
     check_indices(k.cpu().numpy(), idx.cpu().numpy(), ora_k, ora_idx, s32, s64, lens, PS,
                   k_max)
@@ -168,8 +168,8 @@ def test_append_to_a_page_outside_the_cache_writes_nothing():
     mz = mt.copy()
     mz[P] = 0
     s32, s64 = oracle.page_scores(h["q"], mz, btz, lens, PS)
-    ora_k = np.minimum(oracle.budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(lens, ora_k, s32, PS, k_max)
     check_indices(kf.cpu().numpy(), idxf.cpu().numpy(), ora_k, ora_idx, s32, s64, lens, PS,
                   k_max)
@@ -196,8 +196,8 @@ def test_mean_landmark_with_absent_pages():
                                landmark=mean)
     torch.cuda.synchronize()
     s32, s64 = oracle.page_scores_mean(h["q"], ora_sums, btz, lens, PS)
-    ora_k = np.minimum(oracle.budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(lens, PS, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(lens, ora_k, s32, PS, k_max)
     check_indices(k.cpu().numpy(), idx.cpu().numpy(), ora_k, ora_idx, s32, s64, lens, PS,
                   k_max)

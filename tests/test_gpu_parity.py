@@ -16,7 +16,7 @@ from paper_2606_08446_amd import sparrow as S
 from paper_2606_08446_amd import workloads as W
 
 from parity import (SCALE, check_indices, check_meta, check_out, full_check, gpu_run, host, log,
-                    sample_inputs)
+                    oracle_budgets, sample_inputs)
 
 pytestmark = pytest.mark.gpu
 
@@ -113,7 +113,7 @@ def test_random_shapes(seed):
     k_max = S.budget_bound(inp.lens_host, ps, s.bin_tokens, s.min_pages, s.frac_num, s.frac_den)
     if seed % 4 == 3:
         k_max = max(1, k_max // 2)  # a k_max below some budgets: the cap applies
-    full_check(inp, k_max=k_max)
+    full_check(inp, k_max=k_max, capped=seed % 4 == 3)
 
 
 @pytest.mark.parametrize("k_pages", ["one", "n_minus_1", "n", "more"])
@@ -157,7 +157,7 @@ def test_schedule_tables_of_many_bins(n_bins):
 def test_k_max_caps_the_budget():
     log("case k_max cap")
     inp = small_inputs(2, 2, 16, (3000, 5000), seed=8, schedule=W.fraction_budget(1, 2))
-    r = full_check(inp, k_max=40)
+    r = full_check(inp, k_max=40, capped=True)
     assert (r["gpu"]["k"] == 40).all()
 
 
@@ -312,8 +312,8 @@ def sampled_check(inp, seqs, k_max, dense=True, label=""):
     # compare metadata of the sampled pages (GPU meta is indexed by physical page)
     np.testing.assert_array_equal(g["meta"][h["phys"]], ora_meta)
     s32, s64 = oracle.page_scores(h["q"], ora_meta, h["bt"], h["lens"], ps)
-    ora_k = np.minimum(oracle.budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(h["lens"], ora_k, s32, ps, k_max)
     gk = g["k"][list(seqs)]
     gidx = g["idx"][list(seqs)]
@@ -362,7 +362,7 @@ def test_full_size_c4_budget_sweep():
     log("case full-size c4")
     inp = W.generate(W.C4, DEV)
     seqs = pick(inp, 3, 2)
-    for i in (0, 2, 4):
+    for i in range(len(W.C4_FRACTIONS)):   # 2, 5, 10, 25 and 100 % of the pages
         run = W.with_schedule(inp, W.c4_with_fraction(i))
         sampled_check(run, seqs, bound(run), dense=(i == 4), label=run.workload.name)
     del inp

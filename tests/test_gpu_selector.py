@@ -12,7 +12,7 @@ import oracle
 from paper_2606_08446_amd import sparrow as S
 from paper_2606_08446_amd import workloads as W
 
-from parity import NEAR_TIE, SCALE, check_out, host, log, sample_inputs
+from parity import NEAR_TIE, SCALE, check_out, host, log, oracle_budgets, sample_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -94,8 +94,8 @@ def test_mean_selection_and_attention_match_oracle(G, Hkv, ps):
     torch.cuda.synchronize()
     sums = oracle.page_key_sums(h["k"], h["bt"], h["lens"])
     s32, s64 = oracle.page_scores_mean(h["q"], sums, h["bt"], h["lens"], ps)
-    ora_k = np.minimum(oracle.budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(h["lens"], ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(h["lens"], ora_k, s32, ps, k_max)
     check_forced_indices(k.cpu().numpy(), idx.cpu().numpy(), ora_k, ora_idx, s32, s64,
                          h["lens"], ps, 0, 0)
@@ -126,8 +126,8 @@ def test_forced_pages_match_oracle(landmark, sink, local):
     else:
         s32, s64 = oracle.page_scores(h["q"], oracle.page_meta(h["k"], h["bt"], h["lens"]),
                                       h["bt"], h["lens"], 16)
-    ora_k = np.minimum(oracle.budgets(h["lens"], 16, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(h["lens"], 16, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select_forced(h["lens"], ora_k, s32, 16, k_max, sink, local)
     check_forced_indices(k.cpu().numpy(), idx.cpu().numpy(), ora_k, ora_idx, s32, s64,
                          h["lens"], 16, sink, local)
@@ -201,8 +201,8 @@ def test_full_size_c2_mean_landmark_sampled():
     sums = oracle.page_key_sums(hs["k"], hs["bt"], hs["lens"])
     np.testing.assert_array_equal(meta.cpu().numpy()[hs["phys"]], sums)
     s32, s64 = oracle.page_scores_mean(hs["q"], sums, hs["bt"], hs["lens"], 16)
-    ora_k = np.minimum(oracle.budgets(hs["lens"], 16, s.bin_tokens, s.min_pages, s.frac_num,
-                                      s.frac_den), k_max).astype(np.int32)
+    ora_k = oracle_budgets(hs["lens"], 16, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den, k_max)
     ora_idx = oracle.select(hs["lens"], ora_k, s32, 16, k_max)
     check_forced_indices(k.cpu().numpy()[seqs], idx.cpu().numpy()[seqs], ora_k, ora_idx, s32,
                          s64, hs["lens"], 16, 0, 0)

@@ -498,3 +498,22 @@ def test_whole_step_on_planted_hot_pages_keeps_them():
     for b in range(2):
         for h in range(2):
             assert set(inp.hot_host[b][h]) <= set(r["idx"][b, h].tolist())
+
+
+def test_scores_without_the_fp64_copy_are_the_same_fp32_scores():
+    # page_scores(fp64=False) skips only the adjudication copy: identical fp32 bits
+    w = W.small(B=3, Hq=8, Hkv=2, ps=16, lengths=(700, 33, 2100), seed=71)
+    inp = W.generate(w, "cpu", lengths=[700, 33, 2100])
+    q = W.bf16_bits(inp.q)
+    kc = W.bf16_bits(inp.k_cache)
+    bt, lens = inp.block_table.numpy(), inp.seq_lens.numpy()
+    meta = oracle.page_meta(kc, bt, lens)
+    s32, s64 = oracle.page_scores(q, meta, bt, lens, 16)
+    t32, t64 = oracle.page_scores(q, meta, bt, lens, 16, fp64=False)
+    assert t64 is None and s64 is not None
+    np.testing.assert_array_equal(s32.view(np.uint32), t32.view(np.uint32))
+    sums = oracle.page_key_sums(kc, bt, lens)
+    m32, _ = oracle.page_scores_mean(q, sums, bt, lens, 16)
+    n32, n64 = oracle.page_scores_mean(q, sums, bt, lens, 16, fp64=False)
+    assert n64 is None
+    np.testing.assert_array_equal(m32.view(np.uint32), n32.view(np.uint32))

@@ -56,6 +56,27 @@ def test_two_token_closed_form():
         assert abs(oracle.acceptance(t, d)[0] - (1.0 - abs(s(a_) - s(b_)))) < 1e-14
 
 
+def test_masked_entries_drop_out():
+    # a logit of -inf is a token of probability 0 in both rows: the rate equals the rate over
+    # the rest of the vocabulary (runs at the start, in the middle and at the end of the row)
+    a = rows(3, 3000, 21)
+    b = a + rows(3, 3000, 22, scale=0.8)
+    keep = np.ones(3000, bool)
+    keep[:700] = keep[1500:1503] = keep[-129:] = False
+    am, bm = a.copy(), b.copy()
+    am[:, ~keep] = -np.inf
+    bm[:, ~keep] = -np.inf
+    for tau in (1.0, 0.6):
+        want = oracle.acceptance(np.ascontiguousarray(a[:, keep]),
+                                 np.ascontiguousarray(b[:, keep]), tau)
+        np.testing.assert_allclose(oracle.acceptance(am, bm, tau), want, rtol=0, atol=1e-14)
+    # and against the definition on the masked distributions
+    p, q = softmax64(a[:, keep]), softmax64(b[:, keep])
+    np.testing.assert_allclose(oracle.acceptance(am, bm),
+                               [math.fsum(np.minimum(p[t], q[t])) for t in range(3)],
+                               rtol=0, atol=1e-12)
+
+
 def test_shift_and_temperature():
     a, b = rows(3, 4000, 7), rows(3, 4000, 8)
     a, b = np.round(a * 1024) / 1024, np.round(b * 1024) / 1024   # so that shifts are exact
