@@ -262,6 +262,30 @@ int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, cons
                                void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * sparrow_sparse_decode_attn for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation): the same
+ * computation and results, with the workspace taken from a buffer of
+ * SPARROW_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on (from the
+ * first call on that GPU until the process ends).  The call allocates nothing.
+ *
+ * Every call on one GPU uses that GPU's buffer: calls that can overlap on one GPU (on
+ * different streams, or from several host threads without ordering) race and must not be
+ * issued; calls in one stream are ordered and safe.  The buffer needs no initialisation.
+ * Shapes whose workspace (sparrow_workspace_size with SPARROW_OP_SPARSE_ATTN) exceeds
+ * SPARROW_NOALLOC_SCRATCH_BYTES are refused with SPARROW_EWORKSPACE; the Qwen3-shaped decode
+ * batches here need 5-13 MiB.
+ *
+ * Arguments and the other errors are those of sparrow_sparse_decode_attn without the
+ * workspace; SPARROW_EHIP also when the buffer's address cannot be obtained.
+ */
+#define SPARROW_NOALLOC_SCRATCH_BYTES 33554432 /* 32 MiB */
+int sparrow_sparse_decode_attn_noalloc(const sparrow_shape_t *shape, const void *q,
+                                       const void *k_cache, const void *v_cache,
+                                       const int32_t *block_table, const int32_t *seq_lens,
+                                       const int32_t *k, const int32_t *idx, int32_t k_max,
+                                       float scale, void *out, int32_t out_dtype, void *stream);
+
+/*
  * Dense paged decode attention (the dense rollout baseline, Eq. dense-cost):
  * the same as sparrow_sparse_decode_attn with T = every valid token of the
  * sequence.

@@ -173,6 +173,39 @@ int sparrow_sparse_decode_attn(const sparrow_shape_t *shape, const void *q, cons
                                       static_cast<hipStream_t>(stream)));
 }
 
+int sparrow_sparse_decode_attn_noalloc(const sparrow_shape_t *shape, const void *q,
+                                       const void *k_cache, const void *v_cache,
+                                       const int32_t *block_table, const int32_t *seq_lens,
+                                       const int32_t *k, const int32_t *idx, int32_t k_max,
+                                       float scale, void *out, int32_t out_dtype, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !k || !idx || !out)
+        return SPARROW_EINVAL;
+    if (!al16(q) || !al16(k_cache) || !al16(v_cache) || !al4(block_table) || !al4(seq_lens) ||
+        !al4(k) || !al4(idx) || !al16(out))
+        return SPARROW_EINVAL;
+    if (k_max < 1 || k_max > SPARROW_MAX_PAGES_PER_SEQ)
+        return SPARROW_EINVAL;
+    if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
+        return SPARROW_EUNSUPPORTED;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    if (shape->batch > kMaxBatch)
+        return SPARROW_EUNSUPPORTED;
+    const AttnPlan plan = plan_attention(*shape);
+    if (plan.workspace_bytes > kScratchBytes)
+        return SPARROW_EWORKSPACE;
+    void *ws = attention_scratch();
+    if (ws == nullptr)
+        return SPARROW_EHIP;
+    return status_of(launch_attention(*shape, plan, q, k_cache, v_cache, block_table, seq_lens, k,
+                                      idx, k_max, scale, out, out_dtype, ws,
+                                      static_cast<hipStream_t>(stream)));
+}
+
 int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *block_table,
                               const int32_t *seq_lens, float scale, void *out, int32_t out_dtype,

@@ -535,7 +535,30 @@ int device_waves()
     return w;
 }
 
+// Attention workspace that lives in the library, for callers that cannot allocate
+// (sparrow_sparse_decode_attn_noalloc).  Each GPU the library runs on holds one copy of the
+// array until the process ends; host code reaches it only through the address that
+// hipGetSymbolAddress returns on that device (the array's name is a host-side stand-in).
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 }  // namespace
+
+void *attention_scratch()
+{
+    static std::atomic<void *> addr[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return nullptr;
+    void *p = addr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        // once per device, with that device current (concurrent first calls all store the
+        // same address)
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess)
+            return nullptr;
+        addr[dev].store(p, std::memory_order_release);
+    }
+    return p;
+}
 
 AttnPlan plan_attention(const sparrow_shape_t &s)
 {

@@ -204,6 +204,11 @@ struct AttnPlan {
 };
 
 AttnPlan plan_attention(const sparrow_shape_t &s);
+
+// The library's own attention workspace on the current device (kScratchBytes), or nullptr
+// when its address cannot be obtained.
+constexpr size_t kScratchBytes = (size_t)SPARROW_NOALLOC_SCRATCH_BYTES;
+void *attention_scratch();
 hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
                             const void *k_cache, const void *v_cache, const int32_t *block_table,
                             const int32_t *seq_lens, const int32_t *k, const int32_t *idx,

@@ -37,12 +37,13 @@ SPARROW_LOGITS_BF16 = 1
 SPARROW_OP_SCORE_TOPK = 0
 SPARROW_OP_SPARSE_ATTN = 1
 SPARROW_OP_DENSE_ATTN = 2
+SPARROW_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 EXPORTS = ("sparrow_page_meta_update", "sparrow_append_kv", "sparrow_page_score_topk",
            "sparrow_append_score_topk", "sparrow_sparse_decode_attn", "sparrow_dense_decode_attn",
            "sparrow_acceptance_rate", "sparrow_acceptance_rate_topk", "sparrow_tail_stats",
-           "sparrow_stream_read", "sparrow_budget_bound", "sparrow_workspace_size",
-           "sparrow_status_string")
+           "sparrow_stream_read", "sparrow_sparse_decode_attn_noalloc", "sparrow_budget_bound",
+           "sparrow_workspace_size", "sparrow_status_string")
 
 
 class SparrowError(RuntimeError):
@@ -97,7 +98,9 @@ def load():
     lib.sparrow_tail_stats.argtypes = [ctypes.c_int64, _p, _p, _i32, _i32, ctypes.c_double, _p,
                                        _p, _p, _p]
     lib.sparrow_stream_read.argtypes = [_p, ctypes.c_int64, _p, _p]
-    for fn in EXPORTS[:10]:
+    lib.sparrow_sparse_decode_attn_noalloc.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _i32,
+                                                       ctypes.c_float, _p, _i32, _p]
+    for fn in EXPORTS[:11]:
         getattr(lib, fn).restype = ctypes.c_int
     lib.sparrow_budget_bound.argtypes = [_p, ctypes.c_int64, _i32, _i32, _i32, _p, _p, _i32, _p]
     lib.sparrow_budget_bound.restype = ctypes.c_int32
@@ -141,6 +144,13 @@ def sparrow_sparse_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens
     return load().sparrow_sparse_decode_attn(ctypes.byref(shape), q, k_cache, v_cache,
                                              block_table, seq_lens, k, idx, k_max, scale, out,
                                              out_dtype, workspace, ws_bytes, stream)
+
+
+def sparrow_sparse_decode_attn_noalloc(shape, q, k_cache, v_cache, block_table, seq_lens, k, idx,
+                                       k_max, scale, out, out_dtype, stream):
+    return load().sparrow_sparse_decode_attn_noalloc(ctypes.byref(shape), q, k_cache, v_cache,
+                                                     block_table, seq_lens, k, idx, k_max, scale,
+                                                     out, out_dtype, stream)
 
 
 def sparrow_dense_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens, scale, out,

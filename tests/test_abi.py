@@ -353,3 +353,32 @@ def test_stream_read_validates_arguments(lib):
     assert S.sparrow_stream_read(FAKE, 24, FAKE, None) == S.SPARROW_EINVAL   # not a multiple of 16
     assert S.sparrow_stream_read(FAKE + 8, 16, FAKE, None) == S.SPARROW_EINVAL
     assert S.sparrow_stream_read(FAKE, 16, FAKE + 2, None) == S.SPARROW_EINVAL
+
+
+def test_noalloc_attention_validates_arguments(lib):
+    # the workspace-free attention entry point checks its arguments like the one with a
+    # workspace, and refuses shapes whose workspace exceeds the library's buffer
+    shape = good_shape()
+    ok = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, ksel=FAKE, idx=FAKE, k_max=8,
+              out=FAKE, dt=S.SPARROW_OUT_F32)
+
+    def call(shape=shape, **kw):
+        a = dict(ok, **kw)
+        return S.sparrow_sparse_decode_attn_noalloc(shape, a["q"], a["k"], a["v"], a["bt"],
+                                                    a["lens"], a["ksel"], a["idx"], a["k_max"],
+                                                    0.088, a["out"], a["dt"], None)
+    for arg in ("q", "k", "v", "bt", "lens", "ksel", "idx", "out"):
+        assert call(**{arg: None}) == S.SPARROW_EINVAL, arg
+        assert call(**{arg: FAKE + 2}) == S.SPARROW_EINVAL, arg
+    for arg in ("q", "k", "v", "out"):
+        assert call(**{arg: FAKE + 4}) == S.SPARROW_EINVAL, arg
+    assert call(k_max=0) == S.SPARROW_EINVAL
+    assert call(k_max=S.SPARROW_MAX_PAGES_PER_SEQ + 1) == S.SPARROW_EINVAL
+    assert call(dt=7) == S.SPARROW_EUNSUPPORTED
+    assert call(shape=good_shape(batch=0)) == S.SPARROW_OK
+    for kw, status in BAD_SHAPES:
+        assert call(shape=good_shape(**kw)) == status, kw
+    big = S.make_shape(8192, 16, 1, 16, 64, 1 << 20)
+    assert S.sparrow_workspace_size(big, 8, S.SPARROW_OP_SPARSE_ATTN) > \
+        S.SPARROW_NOALLOC_SCRATCH_BYTES
+    assert call(shape=big) == S.SPARROW_EWORKSPACE
