@@ -1,5 +1,6 @@
 """Rollout cost model of Sparrow (arXiv 2606.08446): Eq. dense-cost and Eq. sparse-cost
-(Sec. 3.3, Control Study 2) and the budgeted form of Appendix F, in equivalent FLOPs.
+(Sec. 3.3, Control Study 2) and the budgeted form of Appendix F, in equivalent FLOPs, for a
+fixed budget or summed over a rollout whose budget follows a schedule table (Sec. 3.2).
 
 Both forms add compute to memory traffic weighted by an intensity I (FLOPs that one
 element of memory traffic is worth): I = peak FLOP/s x element bytes / memory bandwidth.
@@ -111,6 +112,60 @@ def decode_step_elements(lengths, budgets_tokens, page_size, d, landmark_vectors
     return dense, sparse
 
 
+def schedule_budget_tokens(lengths, schedule, page_size):
+    """Budget in tokens of sequences of the given lengths under a schedule table (the form
+    the kernels consume: ``(bin_tokens, min_pages, frac_num, frac_den)``): the library's own
+    budget in pages (sparrow_budget_bound, host code) times the page size, capped at the
+    length (a budget covering every page reads every token)."""
+    import numpy as np
+
+    from . import sparrow
+    bin_tokens, min_pages, frac_num, frac_den = schedule
+    lens = np.asarray(lengths, dtype=np.int64)
+    pages, _ = sparrow.budgets(lens, page_size, bin_tokens, min_pages, frac_num, frac_den)
+    return np.minimum(pages.astype(np.int64) * page_size, lens)
+
+
+def rollout_costs(x: Rollout, batch: int, schedule, page_size: int, I: float,
+                  landmark_vectors: int = 2) -> dict:
+    """Per-layer cost of a whole rollout with a length-dependent budget (Appendix F's
+    per-step attention cost summed over the generation, with K taken from the schedule at
+    each step's context length; the scoring term of Eq. sparse-cost per step).
+
+    Step t (t = 0 .. L_out - 1) attends over a context of L_t = L_in + t tokens: dense reads
+    2 L_t D elements of K and V; sparse reads 2 min(L_t, K(L_t)) D, plus ``landmark_vectors``
+    D-vectors per page of landmarks whenever its budget is below L_t.  Compute: 2 P per
+    generated token plus r D per attended element (Appendix F's C_comp).  ``schedule`` None
+    gives the dense rollout.  Returns elements and costs for B N sequences."""
+    import numpy as np
+    B, N, D, Lo, Li = batch, x.samples, x.d, x.l_out, x.l_in
+    L = Li + np.arange(Lo, dtype=np.int64)
+    if schedule is None:
+        k = L
+    else:
+        k = schedule_budget_tokens(L, schedule, page_size)
+    attn = int((2 * k).sum())
+    sparse_steps = k < L
+    score = int((landmark_vectors * -(-L[sparse_steps] // page_size)).sum())
+    comp = 2 * x.params * B * N * Lo + x.r * B * N * D * attn
+    mem = 2 * x.params * Lo + B * N * D * (attn + score)
+    return {"attn_elems": B * N * D * attn, "score_elems": B * N * D * score,
+            "dense_steps": int(Lo - sparse_steps.sum()), "comp": comp, "mem": mem,
+            "total": comp + I * mem}
+
+
+def rollout_speedup(x: Rollout, batch: int, schedule, page_size: int, I: float,
+                    landmark_vectors: int = 2) -> dict:
+    """Predicted dense / sparse rollout cost ratios of a schedule: whole model (Appendix F's
+    total with the weights read once per step) and attention memory only (the part the
+    decode kernels move)."""
+    d = rollout_costs(x, batch, None, page_size, I, landmark_vectors)
+    s = rollout_costs(x, batch, schedule, page_size, I, landmark_vectors)
+    return {"total": d["total"] / s["total"],
+            "attention_memory": d["attn_elems"] / (s["attn_elems"] + s["score_elems"]),
+            "dense": d, "sparse": s}
+
+
 def main():
     ap = argparse.ArgumentParser(description="Sparrow rollout cost model (eFLOPs)")
     ap.add_argument("--model", default="1.7b", choices=sorted(QWEN3))
@@ -122,6 +177,8 @@ def main():
     ap.add_argument("--bandwidth", type=float, default=MI355X_HBM_BYTES_PER_S,
                     help="bytes/s used for I (e.g. a measured copy bandwidth)")
     ap.add_argument("--landmark-vectors", type=int, default=1)
+    ap.add_argument("--schedule", choices=("c1", "c2", "c3", "c4", "c5"),
+                    help="also integrate the rollout with this workload's schedule table")
     a = ap.parse_args()
     m = QWEN3[a.model]
     x = Rollout(m["params"], a.samples, a.l_in, a.l_out, m["d"], m["r"])
@@ -130,9 +187,18 @@ def main():
     s = sparse_cost(x, I, a.budget, a.page_size, a.landmark_vectors)
     fd = appendix_f_costs(x, 1, None, I)
     fs = appendix_f_costs(x, 1, a.budget, I)
-    print(json.dumps({"I": I, "dense": d, "sparse": s, "speedup": d["total"] / s["total"],
-                      "appendix_f": {"dense": fd, "sparse": fs,
-                                     "speedup": fd["total"] / fs["total"]}}))
+    out = {"I": I, "dense": d, "sparse": s, "speedup": d["total"] / s["total"],
+           "appendix_f": {"dense": fd, "sparse": fs, "speedup": fd["total"] / fs["total"]}}
+    if a.schedule:
+        from . import workloads as W
+        w = W.CONFIGS[a.schedule] if a.schedule != "c4" else W.C4
+        sch = w.schedule
+        r = rollout_speedup(x, 1, (sch.bin_tokens, sch.min_pages, sch.frac_num, sch.frac_den),
+                            a.page_size, I, a.landmark_vectors)
+        out["rollout_with_schedule"] = {"schedule_of": w.name, "speedup": r["total"],
+                                        "attention_memory_speedup": r["attention_memory"],
+                                        "dense_steps": r["sparse"]["dense_steps"]}
+    print(json.dumps(out))
 
 
 if __name__ == "__main__":

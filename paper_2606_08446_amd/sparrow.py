@@ -19,7 +19,8 @@ from typing import Optional, Sequence
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libsparrow.so")
+# SPARROW_LIB selects another build of the library (the host-sanitizer build, for instance).
+LIB_PATH = os.environ.get("SPARROW_LIB", os.path.join(_PKG, "libsparrow.so"))
 
 SPARROW_OK = 0
 SPARROW_EINVAL = -1

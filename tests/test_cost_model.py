@@ -84,3 +84,60 @@ def test_decode_step_elements_do_not_overflow_on_numpy_inputs():
     dense, sparse = C.decode_step_elements(lens, budgets, 32, 1024)
     assert dense == 2 * 40960 * 1024 * 256 and sparse > 0 and dense / sparse > 1
 
+
+
+# ---------------------------------------------------------------- rollouts under a schedule
+R = C.Rollout(params=1.7e9, samples=4, l_in=700, l_out=9000, d=1024, r=2)
+
+
+def test_rollout_with_a_constant_table_is_appendix_f_summed_per_step():
+    # a fixed budget of P pages of ps tokens: attention elements per sequence per D are
+    # Appendix F's H(L_in, L_out, K) less its continuous dense phase's extra L_dense
+    # (sum over t < L_dense of 2 (L_in + t) = (2 L_in + L_dense) L_dense - L_dense)
+    for P, ps in ((64, 16), (200, 32), (30, 16), (1000, 16)):
+        K = P * ps
+        r = C.rollout_costs(R, 3, (2048, (P,), (0,), 1), ps, 625.0)
+        ld = C.dense_len(R.l_in, R.l_out, K)
+        assert r["attn_elems"] == 3 * R.samples * R.d * (C.budget_h(R.l_in, R.l_out, K) - ld)
+        # steps that read their whole context: L_t <= K (at L_t = K the budget covers every
+        # page, so no scoring runs; Appendix F's L_dense counts L_t < K, same attention)
+        assert r["dense_steps"] == min(R.l_out, max(0, K - R.l_in + 1))
+
+
+def test_rollout_whose_budget_covers_the_context_is_dense():
+    whole = (2048, (0,), (1,), 1)                 # ceil(n * 1 / 1) = n pages
+    d = C.rollout_costs(R, 2, None, 16, 625.0)
+    s = C.rollout_costs(R, 2, whole, 16, 625.0)
+    assert s == d and s["score_elems"] == 0 and s["dense_steps"] == R.l_out
+    assert C.rollout_speedup(R, 2, whole, 16, 625.0)["total"] == 1.0
+    # the dense rollout: sum over t of 2 (L_in + t) = (2 L_in + L_out) L_out - L_out
+    assert d["attn_elems"] == 2 * R.samples * R.d * \
+        ((2 * R.l_in + R.l_out) * R.l_out - R.l_out)
+
+
+def test_rollout_half_budget_against_brute_force():
+    # one-token pages, half the pages: K(L) = ceil(L / 2); scoring reads 2 landmark vectors
+    # per page (= per token) on every step whose budget is below its context
+    sch = (2048, (0,), (1,), 2)
+    r = C.rollout_costs(R, 1, sch, 1, 625.0)
+    attn = score = 0
+    for t in range(R.l_out):
+        L = R.l_in + t
+        k = max(1, -(-L // 2))
+        attn += 2 * min(L, k)
+        if k < L:
+            score += 2 * L
+    assert r["attn_elems"] == R.samples * R.d * attn
+    assert r["score_elems"] == R.samples * R.d * score
+
+
+def test_rollout_with_a_dense_first_bin():
+    # dense through the first 2048-token bin, 10 % of the pages after it
+    sch = (2048, (0, 0), (10, 1), 10)
+    r = C.rollout_costs(R, 1, sch, 16, 625.0)
+    assert r["dense_steps"] == sum(1 for t in range(R.l_out) if R.l_in + t <= 2048)
+    sp = C.rollout_speedup(R, 1, sch, 16, 625.0)
+    assert 1.0 < sp["attention_memory"] < 10.0
+    # a larger table never costs less
+    more = C.rollout_costs(R, 1, (2048, (0, 0), (10, 2), 10), 16, 625.0)
+    assert more["attn_elems"] >= r["attn_elems"]
