@@ -95,8 +95,8 @@ class Workload:
         return self.num_q_heads // self.num_kv_heads
 
 
-# The five workloads.  The first is the small single-sequence case; the second is
-# the Qwen3-1.7B-shaped layer the headline number is quoted on.
+# The five workloads.  The first is the small single-sequence case; the fourth, the
+# Qwen3-8B-shaped batch of 256 swept over five budgets, is the largest on one GPU.
 C1 = Workload("c1_b1_l4096_fixed32", 1, 16, 8, 16, 4096, 4096, 11, fixed_budget(32),
               sink_scale=4.0,
               description="batch 1, 16/8 heads, 4096 tokens in 16-token pages, fixed 32-page "
