@@ -58,7 +58,15 @@ template <> struct Logit<uint16_t> {
     }
 };
 
-// Running (max, sum of exp(x - max)).
+// 2^x and log2 x on the VALU's transcendental unit (v_exp_f32 / v_log_f32).  The rate is
+// computed in the base-2 domain with the scale ts = |tau| log2(e) folded into each
+// exponent's FMA: 2^(ts x - m) is one v_fma_f32 and one v_exp_f32 per element, and the
+// running maximum is taken on the unscaled values (ts >= 0 preserves their order; a
+// negative tau is handled by negating the logits as they are read).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float log2_hw(float x) { return __builtin_amdgcn_logf(x); }
+
+// Running (max, sum of 2^(ts x - max)) of base-2-scaled logits (max on the scaled scale).
 struct Lse {
     float m, s;
 };
@@ -68,27 +76,29 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b)
     const float m = fmaxf(a.m, b.m);
     if (m == -INFINITY)
         return {m, 0.f};
-    return {m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
+    return {m, a.s * exp2_hw(a.m - m) + b.s * exp2_hw(b.m - m)};
 }
 
+// Adds the unscaled values x (scale ts >= 0) to the running log-sum-exp.
 template <int N>
-__device__ __forceinline__ void lse_add(Lse &r, const float (&x)[N])
+__device__ __forceinline__ void lse_add(Lse &r, const float (&x)[N], float ts)
 {
     float mx = x[0];
 #pragma unroll
     for (int e = 1; e < N; ++e)
         mx = fmaxf(mx, x[e]);
+    mx *= ts;
     if (mx > r.m) {
-        r.s = r.m == -INFINITY ? 0.f : r.s * __expf(r.m - mx);
+        r.s = r.m == -INFINITY ? 0.f : r.s * exp2_hw(r.m - mx);
         r.m = mx;
     }
     // While every entry seen is -inf (masked vocabulary entries), the chunk adds nothing:
-    // exp(x - 0) = 0 for x = -inf, where x - r.m would be -inf - (-inf) = NaN.
+    // 2^(x - 0) = 0 for x = -inf, where x - r.m would be -inf - (-inf) = NaN.
     const float m = r.m == -INFINITY ? 0.f : r.m;
     float s = 0.f;
 #pragma unroll
     for (int e = 0; e < N; ++e)
-        s += __expf(x[e] - m);
+        s += exp2_hw(fmaf(ts, x[e], -m));
     r.s += s;
 }
 
@@ -125,10 +135,18 @@ __device__ void block_lse2(Lse &a, Lse &b, Lse (*s_red)[2])
     }
 }
 
-template <typename T>
+// Logit as read, negated when the inverse temperature is negative (so that the scale ts
+// applied to it is >= 0).
+template <bool kNeg>
+__device__ __forceinline__ float oriented(float x)
+{
+    return kNeg ? -x : x;
+}
+
+template <typename T, bool kNeg>
 __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict__ target,
                                                             const T *__restrict__ draft, int V,
-                                                            float tau, float *__restrict__ alpha)
+                                                            float ts, float *__restrict__ alpha)
 {
     __shared__ Lse s_red[kAccWaves][2];
     __shared__ float s_sum[kAccWaves];
@@ -144,14 +162,16 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
     // ---- pass 1: log-sum-exp of both rows
     Lse a{-INFINITY, 0.f}, b{-INFINITY, 0.f};
     for (int i = tid; i < head; i += kAccThreads) {
-        const float xa[1] = {tau * Logit<T>::at(pr, i)}, xb[1] = {tau * Logit<T>::at(qr, i)};
-        lse_add(a, xa);
-        lse_add(b, xb);
+        const float xa[1] = {oriented<kNeg>(Logit<T>::at(pr, i))};
+        const float xb[1] = {oriented<kNeg>(Logit<T>::at(qr, i))};
+        lse_add(a, xa, ts);
+        lse_add(b, xb, ts);
     }
     for (int i = tail0 + tid; i < V; i += kAccThreads) {
-        const float xa[1] = {tau * Logit<T>::at(pr, i)}, xb[1] = {tau * Logit<T>::at(qr, i)};
-        lse_add(a, xa);
-        lse_add(b, xb);
+        const float xa[1] = {oriented<kNeg>(Logit<T>::at(pr, i))};
+        const float xb[1] = {oriented<kNeg>(Logit<T>::at(qr, i))};
+        lse_add(a, xa, ts);
+        lse_add(b, xb, ts);
     }
     const u32x4_t *pv = reinterpret_cast<const u32x4_t *>(pr + head);
     const u32x4_t *qv = reinterpret_cast<const u32x4_t *>(qr + head);
@@ -170,11 +190,11 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
             Logit<T>::unpack(rb[u], xb);
 #pragma unroll
             for (int e = 0; e < W; ++e) {
-                xa[e] *= tau;
-                xb[e] *= tau;
+                xa[e] = oriented<kNeg>(xa[e]);
+                xb[e] = oriented<kNeg>(xb[e]);
             }
-            lse_add(a, xa);
-            lse_add(b, xb);
+            lse_add(a, xa, ts);
+            lse_add(b, xb, ts);
         }
     }
     for (; v < nvec; v += kAccThreads) {
@@ -183,22 +203,25 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
         Logit<T>::unpack(qv[v], xb);
 #pragma unroll
         for (int e = 0; e < W; ++e) {
-            xa[e] *= tau;
-            xb[e] *= tau;
+            xa[e] = oriented<kNeg>(xa[e]);
+            xb[e] = oriented<kNeg>(xb[e]);
         }
-        lse_add(a, xa);
-        lse_add(b, xb);
+        lse_add(a, xa, ts);
+        lse_add(b, xb, ts);
     }
     block_lse2(a, b, s_red);
-    const float P = a.m + __logf(a.s);
-    const float Q = b.m + __logf(b.s);
+    const float P = a.m + log2_hw(a.s);  // base-2 log-sum-exp of the scaled rows
+    const float Q = b.m + log2_hw(b.s);
 
-    // ---- pass 2: sum of exp(min(tau a - P, tau b - Q)), vectors in reverse order
+    // ---- pass 2: sum of 2^min(ts a - P, ts b - Q) = exp(min(tau a - lse_a, tau b - lse_b)),
+    // vectors in reverse order
     float acc = 0.f;
     for (int i = tid; i < head; i += kAccThreads)
-        acc += __expf(fminf(tau * Logit<T>::at(pr, i) - P, tau * Logit<T>::at(qr, i) - Q));
+        acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(Logit<T>::at(pr, i)), -P),
+                             fmaf(ts, oriented<kNeg>(Logit<T>::at(qr, i)), -Q)));
     for (int i = tail0 + tid; i < V; i += kAccThreads)
-        acc += __expf(fminf(tau * Logit<T>::at(pr, i) - P, tau * Logit<T>::at(qr, i) - Q));
+        acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(Logit<T>::at(pr, i)), -P),
+                             fmaf(ts, oriented<kNeg>(Logit<T>::at(qr, i)), -Q)));
     v = tid;
     for (; v + 3 * kAccThreads < nvec; v += 4 * kAccThreads) {
         u32x4_t ra[4], rb[4];
@@ -214,7 +237,8 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
             Logit<T>::unpack(rb[u], xb);
 #pragma unroll
             for (int e = 0; e < W; ++e)
-                acc += __expf(fminf(tau * xa[e] - P, tau * xb[e] - Q));
+                acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(xa[e]), -P),
+                                     fmaf(ts, oriented<kNeg>(xb[e]), -Q)));
         }
     }
     for (; v < nvec; v += kAccThreads) {
@@ -223,7 +247,8 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
         Logit<T>::unpack(qv[nvec - 1 - v], xb);
 #pragma unroll
         for (int e = 0; e < W; ++e)
-            acc += __expf(fminf(tau * xa[e] - P, tau * xb[e] - Q));
+            acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(xa[e]), -P),
+                                 fmaf(ts, oriented<kNeg>(xb[e]), -Q)));
     }
 #pragma unroll
     for (int x = 1; x < 64; x <<= 1)
@@ -411,14 +436,19 @@ hipError_t launch_acceptance(int64_t T, int V, int dtype, const void *target, co
 {
     // Unused dynamic LDS: with it only one workgroup fits on a CU.
     constexpr size_t kOnePerCu = 96 * 1024;
-    if (dtype == SPARROW_LOGITS_BF16)
-        hipLaunchKernelGGL(k_acceptance<uint16_t>, dim3((unsigned)T), dim3(kAccThreads),
-                           kOnePerCu, stream, static_cast<const uint16_t *>(target),
-                           static_cast<const uint16_t *>(draft), V, tau, alpha);
-    else
-        hipLaunchKernelGGL(k_acceptance<float>, dim3((unsigned)T), dim3(kAccThreads), kOnePerCu,
-                           stream, static_cast<const float *>(target),
-                           static_cast<const float *>(draft), V, tau, alpha);
+    const bool neg = tau < 0.f;
+    const float ts = (neg ? -tau : tau) * 1.44269504088896340736f;  // |tau| log2(e)
+    const dim3 grid((unsigned)T), block(kAccThreads);
+    if (dtype == SPARROW_LOGITS_BF16) {
+        auto k = neg ? k_acceptance<uint16_t, true> : k_acceptance<uint16_t, false>;
+        hipLaunchKernelGGL(k, grid, block, kOnePerCu, stream,
+                           static_cast<const uint16_t *>(target),
+                           static_cast<const uint16_t *>(draft), V, ts, alpha);
+    } else {
+        auto k = neg ? k_acceptance<float, true> : k_acceptance<float, false>;
+        hipLaunchKernelGGL(k, grid, block, kOnePerCu, stream, static_cast<const float *>(target),
+                           static_cast<const float *>(draft), V, ts, alpha);
+    }
     return hipGetLastError();
 }
 

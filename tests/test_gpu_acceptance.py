@@ -36,7 +36,8 @@ def host_rows(t):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("V,tau", [(3000, 1.0), (3001, 1.0), (4099, 0.7), (1, 1.0), (12, 0.0)])
+@pytest.mark.parametrize("V,tau", [(3000, 1.0), (3001, 1.0), (4099, 0.7), (1, 1.0), (12, 0.0),
+                                   (2999, -0.6), (5000, -1.0)])
 def test_acceptance_matches_oracle(dtype, V, tau):
     log(f"case acceptance {dtype} V={V} tau={tau}")
     li = W.generate_logits(W.small_logits(T=37, V=V, seed=3, dtype=dtype), DEV)
