@@ -79,6 +79,9 @@ def parse():
     ap.add_argument("--cold", action="store_true",
                     help="also time each step after flushing the caches (default for batches "
                          "of at most 16 sequences)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="run the decode workload at this batch size instead of its own (lengths "
+                         "drawn the same way; for scaling studies, not the headline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for counter scaling)")
     return ap.parse_args()
@@ -458,6 +461,9 @@ def bench_decode(args):
     ps = runs[0].page_size
     # every step appends one token per sequence: spare pages for all of them
     runs = [dataclasses.replace(w, extra_pages=(total + 1 + ps - 1) // ps + 1) for w in runs]
+    if args.batch > 0:
+        runs = [dataclasses.replace(w, batch=args.batch, name=f"{w.name}_batch{args.batch}")
+                for w in runs]
     base = runs[headline]
     B, Hkv = base.batch, base.num_kv_heads
     L_layers = args.layers
