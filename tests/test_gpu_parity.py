@@ -80,6 +80,40 @@ def test_small_sweep(case):
 
 
 
+# ------------------------------------------------- both scoring workgroup sizes, one selection
+def replicated(inp, reps):
+    """The batch of `inp` repeated `reps` times over the same cache pages (the block-table
+    rows repeat, so every copy of a sequence reads the same physical pages)."""
+    import dataclasses
+    B = inp.workload.batch
+    w = dataclasses.replace(inp.workload, batch=B * reps)
+    return W.Inputs(workload=w, seq_lens=inp.seq_lens.repeat(reps).contiguous(),
+                    block_table=inp.block_table.repeat(reps, 1).contiguous(),
+                    q=inp.q.repeat(reps, 1, 1).contiguous(), k_cache=inp.k_cache,
+                    v_cache=inp.v_cache, min_pages=inp.min_pages, frac_num=inp.frac_num,
+                    lens_host=np.tile(inp.lens_host, reps), pages_host=np.tile(inp.pages_host, reps))
+
+
+@pytest.mark.parametrize("case", [0, 8, 10, 11, 12, 15])
+def test_scoring_workgroup_sizes_select_alike(case):
+    """A small batch is scored in 8-page workgroups; the same sequences repeated until the
+    grid holds 256 or more 32-page workgroups are scored in 32-page ones.  Both selections
+    equal the oracle's, and every copy of a sequence selects exactly the small batch's
+    pages (the scores are bit-identical)."""
+    G, Hkv, ps, lengths, sched = SWEEP[case]
+    inp = small_inputs(G, Hkv, ps, lengths, seed=100 + case, schedule=sched)
+    blocks = -(-inp.max_pages // 32) * len(lengths) * -(-Hkv // 8)
+    reps = -(-256 // blocks)
+    assert blocks < 256 <= blocks * reps
+    log(f"case block sizes {case}: G={G} Hkv={Hkv} ps={ps} lens={lengths} x{reps}")
+    small = full_check(inp)
+    big = full_check(replicated(inp, reps))
+    B = len(lengths)
+    for r in range(reps):
+        assert np.array_equal(big["gpu"]["k"][r * B:(r + 1) * B], small["gpu"]["k"])
+        assert np.array_equal(big["gpu"]["idx"][r * B:(r + 1) * B], small["gpu"]["idx"])
+
+
 # ------------------------------------------------------------------- seeded random shapes
 def random_case(seed):
     """A shape drawn from a seeded generator: group size, KV heads, page size, ragged
