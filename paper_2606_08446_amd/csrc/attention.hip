@@ -36,6 +36,7 @@ constexpr int kAttnThreads = 256;
 constexpr int kAttnWaves = kAttnThreads / 64;
 constexpr int kBatch = 64;        // pages per prefetched page-list batch
 constexpr int kMaxWaves = 4096;   // upper bound of streaming waves (sizes the workspace)
+constexpr int kUnitSegments = 64;  // streaming waves per (sequence, KV head) unit, on average
 
 struct AttnArgs {
     const uint16_t *q;
@@ -224,7 +225,12 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
             a.plan_off[b] = s_off[b];
 
     const int64_t P = (int64_t)s_off[B] * Hkv;
-    const int64_t W = P < a.total_waves ? P : a.total_waves;
+    // One wave per listed page at most, and at most kUnitSegments waves per unit on average:
+    // a unit split over hundreds of one-page waves leaves the merge a long serial chain of
+    // partials (one 4096-token sequence, dense: 33 -> 21 us per step with the cap).
+    int64_t W = P < a.total_waves ? P : a.total_waves;
+    if (W > (int64_t)B * Hkv * kUnitSegments)
+        W = (int64_t)B * Hkv * kUnitSegments;
     const int w = blockIdx.x * kAttnWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (w >= W)
         return;
