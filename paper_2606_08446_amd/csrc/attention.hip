@@ -4,9 +4,11 @@
 //
 // Work split (streaming waves).  All (sequence, KV head, listed page) positions are laid
 // end to end - sequence by sequence, head by head, in list order - and every resident
-// wave takes one equal, contiguous range of them.  A wave streams its range chunk by
-// chunk with the next 16-token chunk's K/V loads always in flight, and the page list is
-// prefetched in batches of 64 pages one batch ahead, across (sequence, head) boundaries.
+// wave takes one equal, contiguous range of them (fewer waves for a small problem: at
+// most one per position and kUnitSegments per unit on average).  A wave streams its
+// range chunk by chunk with the next 16-token chunk's K/V loads always in flight, and the
+// page list is prefetched in batches of 64 pages one batch ahead, across (sequence, head)
+// boundaries.
 // Its online-softmax state is flushed whenever its range leaves a (sequence, KV head):
 // a unit whose pages all fall in one wave is normalised and written to `out` directly;
 // otherwise the wave writes a partial (m, l, o) to segment slot `wave + unit` (unique
