@@ -596,6 +596,18 @@ def bench_decode(args):
         return [sum(ev[j][f].elapsed_time(ev[j][f + 1]) for j in range(count)) / count
                 for f in range(len(fns))]
 
+    def step_times(fn, first, count):
+        """Duration of each step fn(i) on its own (one event between consecutive steps), for
+        the median and tail; a separate pass from the back-to-back timing."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(count + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for j, i in enumerate(range(first, first + count)):
+            fn(i)
+            ev[j + 1].record(stream)
+        torch.cuda.synchronize()
+        return [ev[j].elapsed_time(ev[j + 1]) for j in range(count)]
+
     def captured(fn, i):
         """fn(layer, i, stream) for every layer captured in one graph; a replay callable."""
         g = torch.cuda.CUDAGraph()
@@ -676,6 +688,8 @@ def bench_decode(args):
             phase = dict(zip(names, per_launch(fns, Wm, 1)))   # the step the graph holds
         else:
             phase = dict(zip(names, per_launch(fns, Wm, K)))
+        restore(True)
+        per_step = np.array(step_times(sparse_fn, Wm, K))
         k_host = lay0.step.k.cpu().numpy()
         idx_host = lay0.step.idx.cpu().numpy()
         ms_cold = None
@@ -695,6 +709,8 @@ def bench_decode(args):
              "budget_pages": [int(k_host.min()), int(k_host.max())], "k_max": int(k_max),
              "queries_per_s": round(B * L_layers / (ms_step * 1e-3), 2),
              "ms_per_step": round(ms_step, 5),
+             "p50_ms_per_step": round(float(np.median(per_step)), 5),
+             "p90_ms_per_step": round(float(np.percentile(per_step, 90)), 5),
              "achieved_GBps": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
              "algorithmic_bytes_per_step": {k: int(v) for k, v in by.items()},
              "phase_ms": {k: round(v, 5) for k, v in phase.items()},
@@ -721,13 +737,17 @@ def bench_decode(args):
     dense_fn = captured(Layer.dense, Wm) if args.graph else dense_step
     ms_dense = timed(dense_fn, Wm, K)
     restore(True)
+    dense_steps = np.array(step_times(dense_fn, Wm, K))
+    restore(True)
     dphase = dict(zip(["append", "dense_attn"],
                       per_launch([lambda i: lay0.append_only(i, sp),
                                   lambda i: lay0.dense_attend(i, sp)], Wm, 1 if args.graph else K)))
     dby = dense_bytes(base, lens_last)
     dgbps = sum(dby.values()) * L_layers / (ms_dense * 1e-3) / 1e9
     dense = {"queries_per_s": round(B * L_layers / (ms_dense * 1e-3), 2),
-             "ms_per_step": round(ms_dense, 5), "bytes_per_step": int(sum(dby.values())),
+             "ms_per_step": round(ms_dense, 5),
+             "p50_ms_per_step": round(float(np.median(dense_steps)), 5),
+             "bytes_per_step": int(sum(dby.values())),
              "achieved_GBps": round(dgbps, 1), "hbm_frac": round(dgbps / HBM_PEAK_GBPS, 4),
              "phase_ms": {k: round(v, 5) for k, v in dphase.items()},
              "attention_hbm_frac": round(dby["dense_attn"] / (dphase["dense_attn"] * 1e-3) / 1e9
@@ -754,6 +774,7 @@ def bench_decode(args):
         "steps": K,
         "warmup": Wm,
         "ms_per_step": h["ms_per_step"],
+        "p50_ms_per_step": h["p50_ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
