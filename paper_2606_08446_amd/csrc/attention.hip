@@ -303,6 +303,56 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
         return live;
     };
 
+    // A unit's finished state: written as the output when the unit lies in this wave alone,
+    // else as a partial (segment `wave + unit`) for the merge.
+    auto write_unit = [&](const f32x4_t (&Os)[8], float m, float l, int b, int h,
+                          bool first, bool last) {
+        const int unit = b * Hkv + h;
+        if (lane == 0) {
+            if (first)
+                a.unit_waves[2 * unit] = w;
+            if (last)
+                a.unit_waves[2 * unit + 1] = w;
+        }
+        if (lr >= G)
+            return;
+        if (first && last) {
+            const float inv = l > 0.f ? 1.f / l : 0.f;
+            const int64_t orow = ((int64_t)b * a.num_q_heads + (int64_t)h * G + lr) * kHeadDim;
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    store_out(a.out, a.out_bf16, orow + 32 * lg + 8 * i + c, Os[c][i] * inv);
+        } else {
+            const int64_t seg = (int64_t)w + unit;
+            float *op = a.o_part + (seg * G + lr) * kHeadDim + 32 * lg;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                st16(op + 8 * i, __builtin_bit_cast(
+                                     u32x4_t, (f32x4_t){Os[0][i], Os[1][i], Os[2][i], Os[3][i]}));
+                st16(op + 8 * i + 4, __builtin_bit_cast(u32x4_t, (f32x4_t){Os[4][i], Os[5][i],
+                                                                          Os[6][i], Os[7][i]}));
+            }
+            if (lg == 0) {
+                a.ml_part[(seg * G + lr) * 2 + 0] = m;
+                a.ml_part[(seg * G + lr) * 2 + 1] = l;
+            }
+        }
+    };
+    // Up to two finished units are held in registers until the range ends: on this GPU a
+    // store counts in the wave's in-order memory counter, so a store issued mid-range would
+    // make the next waits on K/V loads wait for its acknowledgement as well (waves with three
+    // unit ends ran ~8 us longer at a 2 % budget).  A third one before the end is written.
+    struct Held {
+        f32x4_t O[8];
+        float m, l;
+        int b, h;
+        bool from_start, ends_unit;
+    };
+    Held held0, held1;
+    int n_held = 0;
+
     Chunk nxt;
     int tok_next = 0;
     bool live_next = issue(bc, 0, nxt, tok_next);
@@ -376,45 +426,31 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
             continue;
         }
         if (bc.ends_unit || !have_next) {
-            // ---- flush the unit's state: the output itself, or a partial for the merge
+            // ---- the unit's state: written at the end of the range (the output itself, or a
+            // partial for the merge), or held until then
             float l_tot = l_run + __shfl_xor(l_run, 16, 64);
             l_tot += __shfl_xor(l_tot, 32, 64);
-            const int unit = bc.b * Hkv + bc.h;
-            if (lane == 0) {
-                if (from_start)
-                    a.unit_waves[2 * unit] = w;
-                if (bc.ends_unit)
-                    a.unit_waves[2 * unit + 1] = w;
-            }
-            if (lr < G) {
-                if (from_start && bc.ends_unit) {
-                    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-                    const int64_t orow =
-                        ((int64_t)bc.b * a.num_q_heads + (int64_t)bc.h * G + lr) * kHeadDim;
-#pragma unroll
-                    for (int c = 0; c < 8; ++c)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            store_out(a.out, a.out_bf16, orow + 32 * lg + 8 * i + c,
-                                      O[c][i] * inv);
-                } else {
-                    const int64_t seg = (int64_t)w + unit;
-                    float *op = a.o_part + (seg * G + lr) * kHeadDim + 32 * lg;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        st16(op + 8 * i, __builtin_bit_cast(
-                                             u32x4_t, (f32x4_t){O[0][i], O[1][i], O[2][i], O[3][i]}));
-                        st16(op + 8 * i + 4, __builtin_bit_cast(u32x4_t, (f32x4_t){O[4][i], O[5][i],
-                                                                                  O[6][i], O[7][i]}));
-                    }
-                    if (lg == 0) {
-                        a.ml_part[(seg * G + lr) * 2 + 0] = m_run;
-                        a.ml_part[(seg * G + lr) * 2 + 1] = l_tot;
-                    }
-                }
-            }
-            if (!have_next)
+            if (!have_next) {
+                write_unit(O, m_run, l_tot, bc.b, bc.h, from_start, bc.ends_unit);
+                if (n_held > 0)
+                    write_unit(held0.O, held0.m, held0.l, held0.b, held0.h, held0.from_start,
+                               held0.ends_unit);
+                if (n_held > 1)
+                    write_unit(held1.O, held1.m, held1.l, held1.b, held1.h, held1.from_start,
+                               held1.ends_unit);
                 break;
+            }
+            if (n_held == 0) {
+                held0 = Held{{O[0], O[1], O[2], O[3], O[4], O[5], O[6], O[7]}, m_run, l_tot, bc.b,
+                             bc.h, from_start, bc.ends_unit};
+                n_held = 1;
+            } else if (n_held == 1) {
+                held1 = Held{{O[0], O[1], O[2], O[3], O[4], O[5], O[6], O[7]}, m_run, l_tot, bc.b,
+                             bc.h, from_start, bc.ends_unit};
+                n_held = 2;
+            } else {
+                write_unit(O, m_run, l_tot, bc.b, bc.h, from_start, bc.ends_unit);
+            }
             m_run = -INFINITY;
             l_run = 0.f;
 #pragma unroll
