@@ -468,6 +468,21 @@ def test_longest_sequence_the_block_table_allows():
     full_check(inp)
 
 
+@pytest.mark.parametrize("out_dtype", [S.SPARROW_OUT_F32, S.SPARROW_OUT_BF16])
+def test_many_units_per_wave(out_dtype):
+    """Several (sequence, KV head) units end inside one streaming wave's range (more units
+    than resident waves, a few pages each): the finished units a wave holds until its range
+    ends, and the ones past what it holds, are all written."""
+    log(f"case many units per wave, out dtype {out_dtype}")
+    rng = np.random.default_rng(33)
+    B = 3000
+    lengths = tuple(int(x) for x in rng.integers(0, 200, size=B))
+    w = W.small(B=B, Hq=8, Hkv=2, ps=16, lengths=lengths, seed=33,
+                schedule=W.fraction_budget(1, 3, floor_pages=1))
+    inp = W.generate(w, DEV, lengths=list(lengths))
+    full_check(inp, out_dtype=out_dtype)
+
+
 def test_largest_batch():
     # SPARROW_MAX_BATCH ragged sequences (many empty or shorter than a page).
     log("case max batch")
