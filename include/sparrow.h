@@ -246,6 +246,14 @@ int sparrow_append_score_topk(const sparrow_shape_t *shape, const void *q, const
  * computed with bf16 operands and fp32 accumulation (the softmax weights are
  * rounded to bf16 before they multiply V).  An empty token set gives a zero
  * row.  out_dtype is SPARROW_OUT_F32 or SPARROW_OUT_BF16.
+ * The order of the fp32 sums depends only on the shape, k_max and the page
+ * lists, so repeated calls give identical results.  A call with at most 256
+ * (sequence, KV head) units, at most 8 query heads per KV head,
+ * k_max * page_size <= 1024 and max_pages_per_seq <= 4096 runs one workgroup
+ * per unit and leaves the workspace untouched; larger calls split the lists
+ * over all resident waves and merge partials kept in the workspace.  With every page listed and k_max
+ * equal to max_pages_per_seq the result equals sparrow_dense_decode_attn's bit
+ * for bit (the dense call's list bound is max_pages_per_seq).
  *
  * Arguments: shape (host); q, k_cache, v_cache, block_table, seq_lens, k
  * (device [batch]), idx (device [batch][num_kv_heads][k_max]);
@@ -288,7 +296,8 @@ int sparrow_sparse_decode_attn_noalloc(const sparrow_shape_t *shape, const void 
 /*
  * Dense paged decode attention (the dense rollout baseline, Eq. dense-cost):
  * the same as sparrow_sparse_decode_attn with T = every valid token of the
- * sequence.
+ * sequence, and max_pages_per_seq in place of k_max when choosing between one
+ * workgroup per unit and the streaming split.
  *
  * Arguments as above, without k/idx/k_max; workspace of at least
  * sparrow_workspace_size(shape, 0, SPARROW_OP_DENSE_ATTN) bytes.

@@ -13,6 +13,8 @@
 // a unit whose pages all fall in one wave is normalised and written to `out` directly;
 // otherwise the wave writes a partial (m, l, o) to segment slot `wave + unit` (unique
 // along the partition) and k_attn_merge combines the partials of that unit.
+// Small problems (a few units with short lists) take k_attn_unit instead: one workgroup per
+// unit, its waves' states merged in LDS, one launch.
 //
 // Per 16-token chunk, one wave computes all G <= 16 query heads of its KV head on MFMA:
 //   QK:  D[t][g] = sum_d K[t][d] q[g][d]  - 4 x mfma_f32_16x16x32_bf16
@@ -198,6 +200,53 @@ __device__ __forceinline__ void fetch_batch_end(const AttnArgs &a, Batch &t)
     }
 }
 
+// One live 16-token chunk into a wave's online-softmax state: logits on MFMA, the running
+// maximum and sum in the log2 domain, O^T += V^T P.  `valid` (>= 1) tokens of the chunk
+// lie inside the sequence; the rest get weight 0 and their V rows are zeroed.
+__device__ __forceinline__ void attend_chunk(Chunk &ch, int valid, const bf16x8_t (&qf)[4],
+                                             float scale_log2, int lg, float &m_run,
+                                             float &l_run, f32x4_t (&O)[8])
+{
+    // ---- logits of 16 tokens x 16 (padded) heads
+    f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ch.k[i]), qf[i],
+                                                    s, 0, 0, 0);
+    float z[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        z[i] = (4 * lg + i < valid) ? s[i] * scale_log2 : -INFINITY;
+    float cm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
+    cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+    const float m_new = fmaxf(m_run, cm);
+    const float alpha = exp2f(m_run - m_new);
+    const uint32_t p01 = pack_bf16(exp2f(z[0] - m_new), exp2f(z[1] - m_new));
+    const uint32_t p23 = pack_bf16(exp2f(z[2] - m_new), exp2f(z[3] - m_new));
+    l_run = l_run * alpha + ((bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23)));
+    m_run = m_new;
+    if (__ballot(alpha != 1.f)) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            O[c] *= alpha;
+    }
+    if (valid < 16) {  // tokens past the length: zero V (cache slots may hold anything)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (4 * lg + j >= valid)
+                ch.v[j] = (u32x4_t){0u, 0u, 0u, 0u};
+    }
+    // ---- O^T += V^T P
+    const s16x4_t pb = __builtin_bit_cast(s16x4_t, (u32x2_t){p01, p23});
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const u32x2_t av = {pair_of(ch.v[0], ch.v[1], c), pair_of(ch.v[2], ch.v[3], c)};
+        O[c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, av), pb,
+                                                         O[c], 0, 0, 0);
+    }
+}
+
 __device__ __forceinline__ void load_q(const AttnArgs &a, int b, int h, int lr, int lg,
                                        bf16x8_t (&qf)[4])
 {
@@ -379,47 +428,8 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
                 load_q(a, bn.b, bn.h, lr, lg, qn);
         }
 
-        if (live) {
-            // ---- logits of 16 tokens x 16 (padded) heads
-            f32x4_t s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ch.k[i]),
-                                                            qf[i], s, 0, 0, 0);
-            const int valid = L - tok0;  // >= 1
-            float z[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                z[i] = (4 * lg + i < valid) ? s[i] * a.scale_log2 : -INFINITY;
-            float cm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
-            cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
-            cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
-            const float m_new = fmaxf(m_run, cm);
-            const float alpha = exp2f(m_run - m_new);
-            const uint32_t p01 = pack_bf16(exp2f(z[0] - m_new), exp2f(z[1] - m_new));
-            const uint32_t p23 = pack_bf16(exp2f(z[2] - m_new), exp2f(z[3] - m_new));
-            l_run = l_run * alpha + ((bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23)));
-            m_run = m_new;
-            if (__ballot(alpha != 1.f)) {
-#pragma unroll
-                for (int c = 0; c < 8; ++c)
-                    O[c] *= alpha;
-            }
-            if (valid < 16) {  // tokens past the length: zero V (cache slots may hold anything)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (4 * lg + j >= valid)
-                        ch.v[j] = (u32x4_t){0u, 0u, 0u, 0u};
-            }
-            // ---- O^T += V^T P
-            const s16x4_t pb = __builtin_bit_cast(s16x4_t, (u32x2_t){p01, p23});
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const u32x2_t av = {pair_of(ch.v[0], ch.v[1], c), pair_of(ch.v[2], ch.v[3], c)};
-                O[c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, av),
-                                                                 pb, O[c], 0, 0, 0);
-            }
-        }
+        if (live)
+            attend_chunk(ch, L - tok0, qf, a.scale_log2, lg, m_run, l_run, O);
 
         if (!last_in_batch) {
             ++ci;
@@ -467,6 +477,173 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_stream(AttnArgs a)
         bn_pending = have_next;
         if (have_next)
             fetch_batch_begin<kSparse>(a, s_off, cur, pos_end, bn, lane);
+    }
+}
+
+// Small problems (few units, short lists): one workgroup per (sequence, KV head) unit.  The
+// unit's list is split evenly over the workgroup's waves and the waves' (m, l, o) states are
+// merged in LDS in wave order, so the output is written with no partials in HBM and no merge
+// launch.  At this size the step is a chain of dependent launches and memory round trips,
+// so the kernel requests the query rows, the length, the budget, the whole page list and the
+// block-table row (staged in LDS) together.  Each wave then streams its pages with the next
+// chunk's loads in flight; a unit's K/V reads are bound by what one compute unit can fetch
+// (about 64 GB/s measured), which is why the path is kept to short lists.
+constexpr int kUnitThreads = 512;
+constexpr int kUnitWaves = kUnitThreads / 64;
+constexpr int kUnitMaxUnits = 256;     // at most one workgroup per compute unit
+constexpr int kUnitMaxTokens = 1024;   // list bound x page size, per unit
+constexpr int kUnitMaxGroup = 8;       // query heads per KV head (sizes the LDS)
+constexpr int kUnitRow = kHeadDim + 4;  // LDS row stride of a wave's o (floats)
+constexpr int kUnitBtLds = 4096;       // widest block-table row (staged in LDS)
+// A list holds at most 64 pages (the smallest page is 16 tokens), one per lane.
+static_assert(kUnitMaxTokens / 16 <= 64, "a unit's list must fit one wave's lanes");
+
+template <bool kSparse>
+__global__ __launch_bounds__(kUnitThreads) void k_attn_unit(AttnArgs a)
+{
+    __shared__ float s_o[kUnitWaves * kUnitMaxGroup * kUnitRow];
+    __shared__ float s_m[kUnitWaves * kUnitMaxGroup];
+    __shared__ float s_l[kUnitWaves * kUnitMaxGroup];
+    __shared__ int32_t s_bt[kUnitBtLds];
+    __shared__ int32_t s_hdr[2];  // length, budget
+    const int Hkv = a.num_kv_heads;
+    const int G = a.num_q_heads / Hkv;  // <= kUnitMaxGroup (checked by the launcher)
+    const int unit = blockIdx.x;
+    const int b = unit / Hkv;
+    const int h = unit - b * Hkv;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int lr = lane & 15;
+    const int lg = lane >> 4;
+    const int ps = a.ps;
+    const int cpp = ps >> 4;  // 16-token chunks per page
+    const int64_t head_elems = (int64_t)ps * kHeadDim;
+
+    // ---- one round trip for everything the K/V loads depend on: the query rows, the
+    // length and the budget, the unit's page list (lane i holds entry i; k_max <= 64 on this
+    // path) and the block-table row, staged in LDS (max_pages <= kUnitBtLds on this path).
+    // The length and the budget are read with relaxed atomic loads so that they are vector
+    // loads: scalar loads would share their wait counter with the kernel-argument loads and
+    // add a round trip of their own.
+    bf16x8_t qf[4];
+    load_q(a, b, h, lr, lg, qf);
+    int entry = -1;
+    if (kSparse && lane < a.k_max)
+        entry = a.idx[((int64_t)b * Hkv + h) * a.k_max + lane];
+    int32_t hdr = 0;
+    if (threadIdx.x < 2) {
+        const int32_t *hp = kSparse && threadIdx.x == 1 ? a.ksel + b : a.seq_lens + b;
+        hdr = __hip_atomic_load(hp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    {
+        int32_t v[kUnitBtLds / kUnitThreads];
+#pragma unroll
+        for (int i = 0; i < kUnitBtLds / kUnitThreads; ++i) {
+            const int t = threadIdx.x + i * kUnitThreads;
+            v[i] = t < a.max_pages ? a.block_table[(int64_t)b * a.max_pages + t] : 0;
+        }
+#pragma unroll
+        for (int i = 0; i < kUnitBtLds / kUnitThreads; ++i) {
+            const int t = threadIdx.x + i * kUnitThreads;
+            if (t < a.max_pages)
+                s_bt[t] = v[i];
+        }
+    }
+    if (threadIdx.x < 2)
+        s_hdr[threadIdx.x] = hdr;
+    __syncthreads();
+
+    const int len_raw = s_hdr[0];
+    const int cnt_raw = s_hdr[1];
+    const int L = clamp_len(len_raw, ps, a.max_pages);
+    const int np = (L + ps - 1) / ps;
+    const int cnt = kSparse ? (cnt_raw < 0 ? 0 : (cnt_raw > a.k_max ? a.k_max : cnt_raw)) : np;
+    const int p0 = (int)((int64_t)wv * cnt / kUnitWaves);
+    const int nw = (int)((int64_t)(wv + 1) * cnt / kUnitWaves) - p0;  // <= 8 pages
+    // lane i < nw describes list position p0 + i
+    const int e = kSparse ? __shfl(entry, p0 + lane, 64) : p0 + lane;
+    int phys = -1, tok_first = 0;
+    if (lane < nw && e >= 0 && e < np) {  // entries outside the sequence: no page
+        phys = s_bt[e];
+        tok_first = e * ps;
+    }
+
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+    f32x4_t O[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+        O[c] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+    // chunk `ci` of the wave's share: page ci / cpp, sub-chunk ci % cpp; a block-table entry
+    // outside the cache is an absent page
+    auto issue = [&](int ci, Chunk &ch, int &tok) -> bool {
+        const int pi = ci / cpp;
+        const int sub = ci - pi * cpp;
+        const int ph = __builtin_amdgcn_readlane(phys, pi);
+        tok = __builtin_amdgcn_readlane(tok_first, pi) + 16 * sub;
+        const bool live = ph >= 0 && ph < a.num_phys && tok < L;
+        if (live) {
+            const int64_t off =
+                ((int64_t)ph * Hkv + h) * head_elems + (int64_t)(16 * sub) * kHeadDim;
+            load_chunk(ch, a.k_cache + off, a.v_cache + off, lr, lg);
+        }
+        return live;
+    };
+    // the wave's chunks in order, the next one's loads in flight
+    const int nch = nw * cpp;
+    Chunk nxt;
+    int tok_next = 0;
+    bool live_next = nch > 0 && issue(0, nxt, tok_next);
+    for (int ci = 0; ci < nch; ++ci) {
+        Chunk ch = nxt;
+        const bool lv = live_next;
+        const int t0 = tok_next;
+        if (ci + 1 < nch)
+            live_next = issue(ci + 1, nxt, tok_next);
+        if (lv)
+            attend_chunk(ch, L - t0, qf, a.scale_log2, lg, m_run, l_run, O);
+    }
+
+    // ---- the waves' states into LDS (lane (g, r) holds head g, channels 32r .. 32r+31)
+    float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    if (lr < G) {
+        float *op = s_o + (wv * kUnitMaxGroup + lr) * kUnitRow + 32 * lg;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            *reinterpret_cast<f32x4_t *>(op + 8 * i) = (f32x4_t){O[0][i], O[1][i], O[2][i], O[3][i]};
+            *reinterpret_cast<f32x4_t *>(op + 8 * i + 4) =
+                (f32x4_t){O[4][i], O[5][i], O[6][i], O[7][i]};
+        }
+        if (lg == 0) {
+            s_m[wv * kUnitMaxGroup + lr] = m_run;
+            s_l[wv * kUnitMaxGroup + lr] = l_tot;
+        }
+    }
+    __syncthreads();
+
+    // ---- merge in wave order: o = sum_w 2^(m_w - M) o_w / sum_w 2^(m_w - M) l_w
+    for (int x = threadIdx.x; x < G * kHeadDim; x += kUnitThreads) {
+        const int g = x / kHeadDim;
+        const int d = x - g * kHeadDim;
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kUnitWaves; ++w)
+            M = fmaxf(M, s_m[w * kUnitMaxGroup + g]);
+        float lsum = 0.f, acc = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll
+            for (int w = 0; w < kUnitWaves; ++w) {
+                const float m = s_m[w * kUnitMaxGroup + g];
+                const float f = m == -INFINITY ? 0.f : exp2f(m - M);  // no pages: weight 0
+                lsum += f * s_l[w * kUnitMaxGroup + g];
+                acc += f * s_o[(w * kUnitMaxGroup + g) * kUnitRow + d];
+            }
+        }
+        const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+        store_out(a.out, a.out_bf16, ((int64_t)b * a.num_q_heads + (int64_t)h * G + g) * kHeadDim + d,
+                  acc * inv);
     }
 }
 
@@ -647,6 +824,21 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     a.out_bf16 = out_dtype == SPARROW_OUT_BF16 ? 1 : 0;
     a.total_waves = device_waves();
     a.scale_log2 = scale * 1.4426950408889634f;
+    // a small problem: one workgroup per unit, merged in LDS (no partials, no merge launch);
+    // the list bound is k_max for a sparse call and the block table's width for a dense one,
+    // so a full-budget sparse call with k_max = that width takes the same path as dense
+    const int64_t units = (int64_t)s.batch * s.num_kv_heads;
+    const int64_t list_bound = idx != nullptr ? k_max : s.max_pages_per_seq;
+    if (units <= kUnitMaxUnits && G <= kUnitMaxGroup &&
+        list_bound * s.page_size <= kUnitMaxTokens && s.max_pages_per_seq <= kUnitBtLds) {
+        if (idx != nullptr)
+            hipLaunchKernelGGL(k_attn_unit<true>, dim3((unsigned)units), dim3(kUnitThreads), 0,
+                               stream, a);
+        else
+            hipLaunchKernelGGL(k_attn_unit<false>, dim3((unsigned)units), dim3(kUnitThreads), 0,
+                               stream, a);
+        return hipGetLastError();
+    }
     const dim3 grid(a.total_waves / kAttnWaves);
     if (idx != nullptr)
         hipLaunchKernelGGL(k_attn_stream<true>, grid, dim3(kAttnThreads), plan.lds_bytes, stream,
