@@ -44,8 +44,11 @@ ENTRY = {
                     ("attention.hip", "common.h", "wave.h")),
     "dense_attn": ("k_attn_stream<dense> + k_attn_merge", ("attention.hip", "common.h", "wave.h")),
     "append_score_topk": ("k_page_score (with append) + k_topk",
-                          ("score_topk.hip", "common.h", "wave.h")),
-    "score_topk": ("k_page_score + k_topk", ("score_topk.hip", "common.h", "wave.h")),
+                          ("score_topk.hip", "topk.h", "common.h", "wave.h")),
+    "score_topk": ("k_page_score + k_topk", ("score_topk.hip", "topk.h", "common.h", "wave.h")),
+    "decode_step": ("k_page_score (with append) + k_select_attn_unit, or + k_topk + "
+                    "k_attn_stream<sparse> + k_attn_merge",
+                    ("score_topk.hip", "attention.hip", "topk.h", "common.h", "wave.h")),
     "append": ("k_append_kv", ("append.hip", "common.h")),
 }
 
@@ -64,9 +67,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample (the single-thread "
                          "run takes half of it)")
-    ap.add_argument("--step", choices=("fused", "separate"), default="fused",
+    ap.add_argument("--step", choices=("fused", "separate", "whole"), default="fused",
                     help="fused: sparrow_append_score_topk + attention; separate: "
-                         "sparrow_append_kv, sparrow_page_score_topk, attention")
+                         "sparrow_append_kv, sparrow_page_score_topk, attention; whole: "
+                         "sparrow_decode_step (one call per step)")
     ap.add_argument("--landmark", choices=("minmax", "mean"), default="minmax",
                     help="page landmark: channel-wise key min/max (default) or mean key")
     ap.add_argument("--sink", type=int, default=0, help="forced sink pages [0, s)")
@@ -468,6 +472,7 @@ def bench_decode(args):
     B, Hkv = base.batch, base.num_kv_heads
     L_layers = args.layers
     fused = args.step == "fused"
+    whole = args.step == "whole"
     landmark = S.SPARROW_LANDMARK_MEAN if args.landmark == "mean" else S.SPARROW_LANDMARK_MINMAX
     stream = torch.cuda.current_stream(dev)
     sp = stream.cuda_stream
@@ -538,6 +543,9 @@ def bench_decode(args):
             self.step.attend(sp, seq_lens=lens_steps[i])
 
         def sparse(self, i, sp):
+            if whole:
+                self.step.decode_step(self.k_new[i], self.v_new[i], sp, seq_lens=lens_steps[i])
+                return
             self.select(i, sp)
             self.attend(i, sp)
 
@@ -675,7 +683,10 @@ def bench_decode(args):
         # ---- per-entry-point durations of layer 0 over the same steps, from the landmarks
         # the timed loop started from
         restore(True)
-        if fused:
+        if whole:
+            names = ["decode_step"]
+            fns = [lambda i: lay0.sparse(i, sp)]
+        elif fused:
             names = ["append_score_topk", "sparse_attn"]
             fns = [lambda i: lay0.select(i, sp), lambda i: lay0.attend(i, sp)]
         else:
@@ -697,7 +708,9 @@ def bench_decode(args):
             restore(True)
             ms_cold = cold_steps(sparse_step, Wm, K)
         by = sparse_bytes(w, lens_last, k_host, idx_host)
-        if fused:
+        if whole:
+            by = {"decode_step": by["append"] + by["score_topk"] + by["sparse_attn"]}
+        elif fused:
             by = {"append_score_topk": by["append"] + by["score_topk"],
                   "sparse_attn": by["sparse_attn"]}
         total_bytes = sum(by.values())
@@ -787,7 +800,8 @@ def bench_decode(args):
                    "budget_pages": h["budget_pages"], "k_max": h["k_max"],
                    "layers": L_layers, "landmark": args.landmark, "sink_pages": args.sink,
                    "local_pages": args.local, "graph": bool(args.graph),
-                   "step": ("append+score+top-k fused, attention" if fused else
+                   "step": ("append+score+top-k+attention in one call" if whole else
+                            "append+score+top-k fused, attention" if fused else
                             "append, score+top-k, attention") +
                            "; one token appended per sequence per step"},
         "achieved_GBps": h["achieved_GBps"],

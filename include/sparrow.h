@@ -94,6 +94,7 @@ extern "C" {
 #define SPARROW_OP_SCORE_TOPK 0
 #define SPARROW_OP_SPARSE_ATTN 1
 #define SPARROW_OP_DENSE_ATTN 2
+#define SPARROW_OP_DECODE_STEP 3
 
 /* Shape of one layer's decode batch (host struct, read during the call only).
    `landmark` selects the page metadata (SPARROW_LANDMARK_*; 0 = min/max), used by the
@@ -294,6 +295,30 @@ int sparrow_sparse_decode_attn_noalloc(const sparrow_shape_t *shape, const void 
                                        float scale, void *out, int32_t out_dtype, void *stream);
 
 /*
+ * One decode step of one layer in one call (the whole sparse step of Sec. 3.3:
+ * append, landmark scores, the schedule's budget of Sec. 3.2, block top-k and
+ * attention over the selected pages): sparrow_append_score_topk - or
+ * sparrow_page_score_topk when k_new and v_new are both NULL - followed by
+ * sparrow_sparse_decode_attn on the selection it made (k = out_k, idx =
+ * out_idx).  Results (caches, meta, out_k, out_idx, out) equal those of the two
+ * calls in sequence bit for bit.  When the attention call would run one
+ * workgroup per unit (see sparrow_sparse_decode_attn), the budget, the top-k
+ * and the attention run in one kernel after the scoring kernel, with the
+ * selection kept on chip: two launches instead of four.
+ *
+ * Arguments: those of the two calls (k_new and v_new both NULL or both set);
+ * workspace of at least sparrow_workspace_size(shape, k_max,
+ * SPARROW_OP_DECODE_STEP) bytes.
+ * Errors: those of the two calls.
+ */
+int sparrow_decode_step(const sparrow_shape_t *shape, const void *q, const void *k_new,
+                        const void *v_new, void *k_cache, void *v_cache, void *meta,
+                        const int32_t *block_table, const int32_t *seq_lens,
+                        const sparrow_schedule_t *schedule, int32_t k_max, float scale,
+                        int32_t *out_k, int32_t *out_idx, void *out, int32_t out_dtype,
+                        void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * Dense paged decode attention (the dense rollout baseline, Eq. dense-cost):
  * the same as sparrow_sparse_decode_attn with T = every valid token of the
  * sequence, and max_pages_per_seq in place of k_max when choosing between one
@@ -405,7 +430,8 @@ int32_t sparrow_budget_bound(const int32_t *seq_lens, int64_t num_seqs, int32_t 
                              const int32_t *frac_num, int32_t frac_den, int32_t *budgets);
 
 /*
- * Workspace bytes needed by one call of `op` (SPARROW_OP_*) with this shape
+ * Workspace bytes needed by one call of `op` (SPARROW_OP_*: SCORE_TOPK for the
+ * two scoring calls, SPARSE_ATTN, DENSE_ATTN, DECODE_STEP) with this shape
  * and k_max (ignored for SPARROW_OP_DENSE_ATTN).  Returns 0 for an invalid or
  * unsupported shape.  The workspace holds scratch results of one call only;
  * calls that run concurrently need separate workspaces.

@@ -38,6 +38,14 @@ bool al4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 int status_of(hipError_t e) { return e == hipSuccess ? SPARROW_OK : SPARROW_EHIP; }
 
+size_t round256(size_t n) { return (n + 255) / 256 * 256; }
+
+// sparrow_decode_step's workspace: the scores, then the attention's workspace.
+size_t decode_step_workspace(const sparrow_shape_t &s)
+{
+    return round256(score_topk_workspace(s)) + plan_attention(s).workspace_bytes;
+}
+
 }  // namespace
 
 extern "C" {
@@ -233,6 +241,60 @@ int sparrow_dense_decode_attn(const sparrow_shape_t *shape, const void *q, const
                                       static_cast<hipStream_t>(stream)));
 }
 
+int sparrow_decode_step(const sparrow_shape_t *shape, const void *q, const void *k_new,
+                        const void *v_new, void *k_cache, void *v_cache, void *meta,
+                        const int32_t *block_table, const int32_t *seq_lens,
+                        const sparrow_schedule_t *schedule, int32_t k_max, float scale,
+                        int32_t *out_k, int32_t *out_idx, void *out, int32_t out_dtype,
+                        void *workspace, size_t ws_bytes, void *stream)
+{
+    const int rc = check_shape(shape);
+    if (rc != SPARROW_OK)
+        return rc;
+    if (!q || !k_cache || !v_cache || !meta || !block_table || !seq_lens || !schedule || !out_k ||
+        !out_idx || !out || (k_new == nullptr) != (v_new == nullptr))
+        return SPARROW_EINVAL;
+    if (!al16(q) || !al16(k_new) || !al16(v_new) || !al16(k_cache) || !al16(v_cache) ||
+        !al16(meta) || !al4(block_table) || !al4(seq_lens) || !al4(out_k) || !al4(out_idx) ||
+        !al16(out) || !al16(workspace))
+        return SPARROW_EINVAL;
+    if (k_max < 1 || k_max > SPARROW_MAX_PAGES_PER_SEQ || schedule->bin_tokens < 1 ||
+        schedule->n_bins < 1 || schedule->frac_den < 1 || !schedule->min_pages ||
+        !schedule->frac_num || schedule->sink_pages < 0 || schedule->local_pages < 0)
+        return SPARROW_EINVAL;
+    if (out_dtype != SPARROW_OUT_F32 && out_dtype != SPARROW_OUT_BF16)
+        return SPARROW_EUNSUPPORTED;
+    if (shape->batch == 0)
+        return SPARROW_OK;
+    if ((int64_t)shape->batch * shape->num_kv_heads > 65535)
+        return SPARROW_EINVAL;
+    if (shape->batch > kMaxBatch)
+        return SPARROW_EUNSUPPORTED;
+    if (!workspace || ws_bytes < decode_step_workspace(*shape))
+        return SPARROW_EWORKSPACE;
+    const Sched sched{schedule->bin_tokens, schedule->n_bins,     schedule->frac_den,
+                      schedule->min_pages,  schedule->frac_num, schedule->sink_pages,
+                      schedule->local_pages};
+    const AppendArgs app{k_new, v_new, k_new ? k_cache : nullptr, k_new ? v_cache : nullptr};
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    float *scores = static_cast<float *>(workspace);
+    void *attn_ws = static_cast<char *>(workspace) + round256(score_topk_workspace(*shape));
+    hipError_t e = launch_page_score(*shape, q, meta, block_table, seq_lens, sched, k_max, scores,
+                                     app, st);
+    if (e != hipSuccess)
+        return SPARROW_EHIP;
+    if (attention_unit_path(*shape, k_max))
+        return status_of(launch_select_attention(*shape, q, k_cache, v_cache, block_table,
+                                                 seq_lens, sched, k_max, scores, out_k, out_idx,
+                                                 scale, out, out_dtype, st));
+    e = launch_topk(*shape, seq_lens, sched, k_max, scores, out_k, out_idx, st);
+    if (e != hipSuccess)
+        return SPARROW_EHIP;
+    return status_of(launch_attention(*shape, plan_attention(*shape), q, k_cache, v_cache,
+                                      block_table, seq_lens, out_k, out_idx, k_max, scale, out,
+                                      out_dtype, attn_ws, st));
+}
+
 int sparrow_acceptance_rate(int64_t num_tokens, int32_t vocab, int32_t logits_dtype,
                             const void *target_logits, const void *draft_logits,
                             float inv_temperature, float *alpha, void *stream)
@@ -342,6 +404,10 @@ size_t sparrow_workspace_size(const sparrow_shape_t *shape, int32_t k_max, int32
                    : plan_attention(*shape).workspace_bytes;
     case SPARROW_OP_DENSE_ATTN:
         return shape->batch > kMaxBatch ? 0 : plan_attention(*shape).workspace_bytes;
+    case SPARROW_OP_DECODE_STEP:
+        return k_max < 1 || k_max > SPARROW_MAX_PAGES_PER_SEQ || shape->batch > kMaxBatch
+                   ? 0
+                   : decode_step_workspace(*shape);
     default: return 0;
     }
 }

@@ -31,6 +31,7 @@
 #include <atomic>
 
 #include "common.h"
+#include "topk.h"
 #include "wave.h"
 
 namespace sparrow {
@@ -498,19 +499,18 @@ constexpr int kUnitBtLds = 4096;       // widest block-table row (staged in LDS)
 // A list holds at most 64 pages (the smallest page is 16 tokens), one per lane.
 static_assert(kUnitMaxTokens / 16 <= 64, "a unit's list must fit one wave's lanes");
 
-template <bool kSparse>
-__global__ __launch_bounds__(kUnitThreads) void k_attn_unit(AttnArgs a)
+// The attention of one unit over the `cnt` pages of its list, by the workgroup's waves, with
+// the output written: wave w streams list positions [w cnt / 8, (w + 1) cnt / 8), and the
+// waves' (m, l, o) states are merged in LDS in wave order.  entry_of(p) gives the logical
+// page at list position p (every lane calls it; positions past the list are ignored).  The
+// block-table row is in s_bt; s_o, s_m, s_l are the merge's LDS.
+template <typename EntryOf>
+__device__ __forceinline__ void unit_attend(const AttnArgs &a, int b, int h, int L, int cnt,
+                                            const bf16x8_t (&qf)[4], const int32_t *s_bt,
+                                            float *s_o, float *s_m, float *s_l, EntryOf entry_of)
 {
-    __shared__ float s_o[kUnitWaves * kUnitMaxGroup * kUnitRow];
-    __shared__ float s_m[kUnitWaves * kUnitMaxGroup];
-    __shared__ float s_l[kUnitWaves * kUnitMaxGroup];
-    __shared__ int32_t s_bt[kUnitBtLds];
-    __shared__ int32_t s_hdr[2];  // length, budget
     const int Hkv = a.num_kv_heads;
     const int G = a.num_q_heads / Hkv;  // <= kUnitMaxGroup (checked by the launcher)
-    const int unit = blockIdx.x;
-    const int b = unit / Hkv;
-    const int h = unit - b * Hkv;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int lr = lane & 15;
@@ -518,50 +518,11 @@ __global__ __launch_bounds__(kUnitThreads) void k_attn_unit(AttnArgs a)
     const int ps = a.ps;
     const int cpp = ps >> 4;  // 16-token chunks per page
     const int64_t head_elems = (int64_t)ps * kHeadDim;
-
-    // ---- one round trip for everything the K/V loads depend on: the query rows, the
-    // length and the budget, the unit's page list (lane i holds entry i; k_max <= 64 on this
-    // path) and the block-table row, staged in LDS (max_pages <= kUnitBtLds on this path).
-    // The length and the budget are read with relaxed atomic loads so that they are vector
-    // loads: scalar loads would share their wait counter with the kernel-argument loads and
-    // add a round trip of their own.
-    bf16x8_t qf[4];
-    load_q(a, b, h, lr, lg, qf);
-    int entry = -1;
-    if (kSparse && lane < a.k_max)
-        entry = a.idx[((int64_t)b * Hkv + h) * a.k_max + lane];
-    int32_t hdr = 0;
-    if (threadIdx.x < 2) {
-        const int32_t *hp = kSparse && threadIdx.x == 1 ? a.ksel + b : a.seq_lens + b;
-        hdr = __hip_atomic_load(hp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    {
-        int32_t v[kUnitBtLds / kUnitThreads];
-#pragma unroll
-        for (int i = 0; i < kUnitBtLds / kUnitThreads; ++i) {
-            const int t = threadIdx.x + i * kUnitThreads;
-            v[i] = t < a.max_pages ? a.block_table[(int64_t)b * a.max_pages + t] : 0;
-        }
-#pragma unroll
-        for (int i = 0; i < kUnitBtLds / kUnitThreads; ++i) {
-            const int t = threadIdx.x + i * kUnitThreads;
-            if (t < a.max_pages)
-                s_bt[t] = v[i];
-        }
-    }
-    if (threadIdx.x < 2)
-        s_hdr[threadIdx.x] = hdr;
-    __syncthreads();
-
-    const int len_raw = s_hdr[0];
-    const int cnt_raw = s_hdr[1];
-    const int L = clamp_len(len_raw, ps, a.max_pages);
     const int np = (L + ps - 1) / ps;
-    const int cnt = kSparse ? (cnt_raw < 0 ? 0 : (cnt_raw > a.k_max ? a.k_max : cnt_raw)) : np;
     const int p0 = (int)((int64_t)wv * cnt / kUnitWaves);
     const int nw = (int)((int64_t)(wv + 1) * cnt / kUnitWaves) - p0;  // <= 8 pages
     // lane i < nw describes list position p0 + i
-    const int e = kSparse ? __shfl(entry, p0 + lane, 64) : p0 + lane;
+    const int e = entry_of(p0 + lane);
     int phys = -1, tok_first = 0;
     if (lane < nw && e >= 0 && e < np) {  // entries outside the sequence: no page
         phys = s_bt[e];
@@ -645,6 +606,175 @@ __global__ __launch_bounds__(kUnitThreads) void k_attn_unit(AttnArgs a)
         store_out(a.out, a.out_bf16, ((int64_t)b * a.num_q_heads + (int64_t)h * G + g) * kHeadDim + d,
                   acc * inv);
     }
+}
+
+// The block-table row of sequence b into LDS (max_pages <= kUnitBtLds): every load is issued
+// before the first store waits on one.
+__device__ __forceinline__ void stage_block_table(const AttnArgs &a, int b, int32_t *s_bt)
+{
+    int32_t v[kUnitBtLds / kUnitThreads];
+#pragma unroll
+    for (int i = 0; i < kUnitBtLds / kUnitThreads; ++i) {
+        const int t = threadIdx.x + i * kUnitThreads;
+        v[i] = t < a.max_pages ? a.block_table[(int64_t)b * a.max_pages + t] : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < kUnitBtLds / kUnitThreads; ++i) {
+        const int t = threadIdx.x + i * kUnitThreads;
+        if (t < a.max_pages)
+            s_bt[t] = v[i];
+    }
+}
+
+template <bool kSparse>
+__global__ __launch_bounds__(kUnitThreads) void k_attn_unit(AttnArgs a)
+{
+    __shared__ float s_o[kUnitWaves * kUnitMaxGroup * kUnitRow];
+    __shared__ float s_m[kUnitWaves * kUnitMaxGroup];
+    __shared__ float s_l[kUnitWaves * kUnitMaxGroup];
+    __shared__ int32_t s_bt[kUnitBtLds];
+    __shared__ int32_t s_hdr[2];  // length, budget
+    const int Hkv = a.num_kv_heads;
+    const int unit = blockIdx.x;
+    const int b = unit / Hkv;
+    const int h = unit - b * Hkv;
+    const int lane = threadIdx.x & 63;
+
+    // ---- one round trip for everything the K/V loads depend on: the query rows, the
+    // length and the budget, the unit's page list (lane i holds entry i; k_max <= 64 on this
+    // path) and the block-table row, staged in LDS (max_pages <= kUnitBtLds on this path).
+    // The length and the budget are read with relaxed atomic loads so that they are vector
+    // loads: scalar loads would share their wait counter with the kernel-argument loads and
+    // add a round trip of their own.
+    bf16x8_t qf[4];
+    load_q(a, b, h, lane & 15, lane >> 4, qf);
+    int entry = -1;
+    if (kSparse && lane < a.k_max)
+        entry = a.idx[((int64_t)b * Hkv + h) * a.k_max + lane];
+    int32_t hdr = 0;
+    if (threadIdx.x < 2) {
+        const int32_t *hp = kSparse && threadIdx.x == 1 ? a.ksel + b : a.seq_lens + b;
+        hdr = __hip_atomic_load(hp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    stage_block_table(a, b, s_bt);
+    if (threadIdx.x < 2)
+        s_hdr[threadIdx.x] = hdr;
+    __syncthreads();
+
+    const int L = clamp_len(s_hdr[0], a.ps, a.max_pages);
+    const int np = (L + a.ps - 1) / a.ps;
+    const int c = s_hdr[1];
+    const int cnt = kSparse ? (c < 0 ? 0 : (c > a.k_max ? a.k_max : c)) : np;
+    unit_attend(a, b, h, L, cnt, qf, s_bt, s_o, s_m, s_l,
+                [&](int p) { return kSparse ? __shfl(entry, p, 64) : p; });
+}
+
+// Small problems, after the scoring kernel (sparrow_decode_step): the budget, the top-k and
+// the attention of one unit in one workgroup.  The selection stays in LDS - it is written to
+// out_k / out_idx as well, as k_topk writes them - so the step needs no top-k launch and no
+// page-list round trip.  The selection is k_topk's (block_topk on the same keys) and the
+// attention k_attn_unit's (unit_attend on the same list), so the results equal those of the
+// separate calls bit for bit.
+constexpr int kUnitMaxList = kUnitMaxTokens / 16;  // pages in a unit's list, at most
+
+struct SelectArgs {
+    const float *scores;  // [batch][num_kv_heads][max_pages], from the scoring kernel
+    Sched sched;
+    int32_t *out_k;
+    int32_t *out_idx;
+};
+
+__global__ __launch_bounds__(kUnitThreads) void k_select_attn_unit(AttnArgs a, SelectArgs sel)
+{
+    // s_o holds the top-k keys first (n <= kUnitBtLds of them), then the waves' o
+    __shared__ float s_o[kUnitWaves * kUnitMaxGroup * kUnitRow];
+    __shared__ float s_m[kUnitWaves * kUnitMaxGroup];
+    __shared__ float s_l[kUnitWaves * kUnitMaxGroup];
+    __shared__ int32_t s_bt[kUnitBtLds];
+    __shared__ int32_t s_tab[2][kUnitThreads];  // the schedule's tables, when they fit
+    __shared__ int32_t s_sel[kUnitMaxList];
+    __shared__ int32_t s_len;
+    __shared__ TopkLds t;
+    static_assert(kUnitWaves * kUnitMaxGroup * kUnitRow >= kUnitBtLds, "the keys fit s_o");
+    constexpr int kPer = kUnitBtLds / kUnitThreads;  // scores per thread
+    const int Hkv = a.num_kv_heads;
+    const int unit = blockIdx.x;
+    const int b = unit / Hkv;
+    const int h = unit - b * Hkv;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const Sched &sc = sel.sched;
+
+    // ---- one round trip: the query rows, the length (a vector load, as in k_attn_unit), the
+    // schedule's tables, the unit's scores up to the block table's width (entries past the
+    // sequence are never used) and the block-table row
+    bf16x8_t qf[4];
+    load_q(a, b, h, lane & 15, lane >> 4, qf);
+    int32_t len = 0;
+    if (tid == 0)
+        len = __hip_atomic_load(a.seq_lens + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool tab_lds = sc.n_bins <= kUnitThreads;
+    int32_t t_min = 0, t_frac = 0;
+    if (tab_lds && tid < sc.n_bins) {
+        t_min = sc.min_pages[tid];
+        t_frac = sc.frac_num[tid];
+    }
+    const float *src = sel.scores + (int64_t)unit * a.max_pages;
+    float v[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int i = tid + kUnitThreads * j;
+        v[j] = i < a.max_pages ? src[i] : 0.f;
+    }
+    stage_block_table(a, b, s_bt);
+    if (tab_lds && tid < sc.n_bins) {
+        s_tab[0][tid] = t_min;
+        s_tab[1][tid] = t_frac;
+    }
+    if (tid == 0)
+        s_len = len;
+    __syncthreads();
+
+    // ---- budget (capped at k_max <= kUnitMaxList) and selection into s_sel
+    const int L = clamp_len(s_len, a.ps, a.max_pages);
+    const int n = (L + a.ps - 1) / a.ps;
+    int k;
+    if (tab_lds) {
+        const int bin = L > 0 ? budget_bin(L, sc) : 0;
+        k = L > 0 ? budget_from(L, a.ps, s_tab[0][bin], s_tab[1][bin], sc.frac_den, a.k_max) : 0;
+    } else {
+        k = budget_pages(L, a.ps, sc, a.k_max);
+    }
+    if (h == 0 && tid == 0)
+        sel.out_k[b] = k;
+    if (k >= n) {  // every page kept (k == n <= kUnitMaxList; also n == 0)
+        if (tid < n)
+            s_sel[tid] = tid;
+    } else {
+        uint32_t *keys = reinterpret_cast<uint32_t *>(s_o);
+        uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int i = tid + kUnitThreads * j;
+            if (i < n) {
+                // forced pages (sinks, most recent pages) outrank every score
+                const bool forced = i < sc.sink_pages || i >= n - sc.local_pages;
+                const uint32_t key = forced ? 0xffffffffu : score_key(v[j]);
+                keys[i] = key;
+                kmin = min(kmin, key);
+                kmax = max(kmax, key);
+            }
+        }
+        block_topk<kUnitThreads>(keys, n, k, kmin, kmax, t,
+                                 [&](uint32_t pos, int i) { s_sel[pos] = i; });
+    }
+    __syncthreads();  // s_sel complete; the keys are dead, s_o is free for the merge
+
+    int32_t *row = sel.out_idx + (int64_t)unit * a.k_max;
+    for (int i = tid; i < a.k_max; i += kUnitThreads)
+        row[i] = i < k ? s_sel[i] : -1;
+    unit_attend(a, b, h, L, k, qf, s_bt, s_o, s_m, s_l,
+                [&](int p) { return s_sel[p < kUnitMaxList ? p : kUnitMaxList - 1]; });
 }
 
 // Merges the partials of a query-head row whose (sequence, KV head) unit spans several waves,
@@ -794,11 +924,12 @@ AttnPlan plan_attention(const sparrow_shape_t &s)
     return p;
 }
 
-hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
-                            const void *k_cache, const void *v_cache, const int32_t *block_table,
-                            const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
-                            int32_t k_max, float scale, void *out, int out_dtype,
-                            void *workspace, hipStream_t stream)
+namespace {
+
+AttnArgs make_args(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
+                   const void *k_cache, const void *v_cache, const int32_t *block_table,
+                   const int32_t *seq_lens, const int32_t *k, const int32_t *idx, int32_t k_max,
+                   float scale, void *out, int out_dtype, void *workspace)
 {
     const int G = s.num_q_heads / s.num_kv_heads;
     AttnArgs a;
@@ -810,9 +941,13 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     a.ksel = k;
     a.idx = idx;
     a.plan_off = static_cast<int32_t *>(workspace);
-    a.unit_waves = a.plan_off + ((size_t)(s.batch + 1) + 63) / 64 * 64;
-    a.o_part = reinterpret_cast<float *>(static_cast<char *>(workspace) + plan.plan_bytes);
-    a.ml_part = a.o_part + plan.segments * G * kHeadDim;
+    a.unit_waves = a.plan_off == nullptr
+                       ? nullptr
+                       : a.plan_off + ((size_t)(s.batch + 1) + 63) / 64 * 64;
+    a.o_part = workspace == nullptr
+                   ? nullptr
+                   : reinterpret_cast<float *>(static_cast<char *>(workspace) + plan.plan_bytes);
+    a.ml_part = a.o_part == nullptr ? nullptr : a.o_part + plan.segments * G * kHeadDim;
     a.out = out;
     a.k_max = k_max;
     a.batch = s.batch;
@@ -824,13 +959,31 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     a.out_bf16 = out_dtype == SPARROW_OUT_BF16 ? 1 : 0;
     a.total_waves = device_waves();
     a.scale_log2 = scale * 1.4426950408889634f;
-    // a small problem: one workgroup per unit, merged in LDS (no partials, no merge launch);
-    // the list bound is k_max for a sparse call and the block table's width for a dense one,
-    // so a full-budget sparse call with k_max = that width takes the same path as dense
+    return a;
+}
+
+}  // namespace
+
+// A small problem: one workgroup per unit, merged in LDS (no partials, no merge launch).  The
+// list bound is k_max for a sparse call and the block table's width for a dense one, so a
+// full-budget sparse call with k_max = that width takes the same path as the dense call.
+bool attention_unit_path(const sparrow_shape_t &s, int64_t list_bound)
+{
+    const int G = s.num_q_heads / s.num_kv_heads;
+    return (int64_t)s.batch * s.num_kv_heads <= kUnitMaxUnits && G <= kUnitMaxGroup &&
+           list_bound * s.page_size <= kUnitMaxTokens && s.max_pages_per_seq <= kUnitBtLds;
+}
+
+hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, const void *q,
+                            const void *k_cache, const void *v_cache, const int32_t *block_table,
+                            const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
+                            int32_t k_max, float scale, void *out, int out_dtype,
+                            void *workspace, hipStream_t stream)
+{
+    const AttnArgs a = make_args(s, plan, q, k_cache, v_cache, block_table, seq_lens, k, idx,
+                                 k_max, scale, out, out_dtype, workspace);
     const int64_t units = (int64_t)s.batch * s.num_kv_heads;
-    const int64_t list_bound = idx != nullptr ? k_max : s.max_pages_per_seq;
-    if (units <= kUnitMaxUnits && G <= kUnitMaxGroup &&
-        list_bound * s.page_size <= kUnitMaxTokens && s.max_pages_per_seq <= kUnitBtLds) {
+    if (attention_unit_path(s, idx != nullptr ? k_max : s.max_pages_per_seq)) {
         if (idx != nullptr)
             hipLaunchKernelGGL(k_attn_unit<true>, dim3((unsigned)units), dim3(kUnitThreads), 0,
                                stream, a);
@@ -852,6 +1005,22 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
     const int rows = s.batch * s.num_q_heads;
     hipLaunchKernelGGL(k_attn_merge, dim3((rows + kMergeRows - 1) / kMergeRows),
                        dim3(kMergeThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_attention(const sparrow_shape_t &s, const void *q, const void *k_cache,
+                                   const void *v_cache, const int32_t *block_table,
+                                   const int32_t *seq_lens, const Sched &sched, int32_t k_max,
+                                   const float *scores, int32_t *out_k, int32_t *out_idx,
+                                   float scale, void *out, int out_dtype, hipStream_t stream)
+{
+    AttnPlan none{};
+    const AttnArgs a = make_args(s, none, q, k_cache, v_cache, block_table, seq_lens, out_k,
+                                 out_idx, k_max, scale, out, out_dtype, nullptr);
+    const SelectArgs sel{scores, sched, out_k, out_idx};
+    const int64_t units = (int64_t)s.batch * s.num_kv_heads;
+    hipLaunchKernelGGL(k_select_attn_unit, dim3((unsigned)units), dim3(kUnitThreads), 0, stream,
+                       a, sel);
     return hipGetLastError();
 }
 

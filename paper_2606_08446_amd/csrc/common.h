@@ -179,6 +179,17 @@ struct AppendArgs {
 };
 
 size_t score_topk_workspace(const sparrow_shape_t &s);
+// Scores of every page into `scores` [batch][num_kv_heads][max_pages] (with the append when
+// app.k_new != nullptr); sequences whose budget keeps every page are skipped.
+hipError_t launch_page_score(const sparrow_shape_t &s, const void *q, void *meta,
+                             const int32_t *block_table, const int32_t *seq_lens,
+                             const Sched &sched, int32_t k_max, float *scores,
+                             const AppendArgs &app, hipStream_t stream);
+// Budgets and top-k page lists from the scores.
+hipError_t launch_topk(const sparrow_shape_t &s, const int32_t *seq_lens, const Sched &sched,
+                       int32_t k_max, const float *scores, int32_t *out_k, int32_t *out_idx,
+                       hipStream_t stream);
+// Both of the above.
 hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta,
                              const int32_t *block_table, const int32_t *seq_lens,
                              const Sched &sched, int32_t k_max, int32_t *out_k,
@@ -214,5 +225,15 @@ hipError_t launch_attention(const sparrow_shape_t &s, const AttnPlan &plan, cons
                             const int32_t *seq_lens, const int32_t *k, const int32_t *idx,
                             int32_t k_max, float scale, void *out, int out_dtype,
                             void *workspace, hipStream_t stream);
+// Whether attention with this list bound (k_max, or max_pages_per_seq for dense) runs one
+// workgroup per (sequence, KV head) unit.
+bool attention_unit_path(const sparrow_shape_t &s, int64_t list_bound);
+// Budgets, top-k and sparse attention of a problem on the unit path, from the scoring
+// kernel's scores, in one launch (writes out_k, out_idx and out).
+hipError_t launch_select_attention(const sparrow_shape_t &s, const void *q, const void *k_cache,
+                                   const void *v_cache, const int32_t *block_table,
+                                   const int32_t *seq_lens, const Sched &sched, int32_t k_max,
+                                   const float *scores, int32_t *out_k, int32_t *out_idx,
+                                   float scale, void *out, int out_dtype, hipStream_t stream);
 
 }  // namespace sparrow

@@ -18,6 +18,7 @@
 // threshold T and how many keys equal to T to keep; one block scan of (count > T,
 // count == T) then places every kept page at its rank in ascending page order.
 #include "common.h"
+#include "topk.h"
 #include "wave.h"
 
 namespace sparrow {
@@ -317,26 +318,14 @@ __global__ __launch_bounds__(kScoreThreads) void k_page_score(
     }
 }
 
-// fp32 score -> uint32 whose unsigned order is the order of the scores (-0 == +0).
-__device__ __forceinline__ uint32_t score_key(float s)
-{
-    uint32_t u = __float_as_uint(s);
-    if (u == 0x80000000u)
-        u = 0u;
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
 template <int kTopkThreads>
 __global__ __launch_bounds__(kTopkThreads) void k_topk(
     const float *__restrict__ scores, const int32_t *__restrict__ seq_lens, Sched sched,
     int k_max, int num_kv_heads, int ps, int max_pages, int32_t *__restrict__ out_k,
     int32_t *__restrict__ out_idx)
 {
-    constexpr int kTopkWaves = kTopkThreads / 64;
     extern __shared__ uint32_t keys[];  // [max_pages]
-    __shared__ uint32_t hist[2][256];
-    __shared__ uint32_t red_a[kTopkWaves], red_b[kTopkWaves], red_c[kTopkWaves];
-    __shared__ uint32_t s_digit, s_rem, s_done;
+    __shared__ TopkLds t;
 
     const int unit = blockIdx.x;
     const int b = unit / num_kv_heads;
@@ -344,8 +333,6 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
     const int L = clamp_len(seq_lens[b], ps, max_pages);
     const int n = (L + ps - 1) / ps;
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
     int32_t *row = out_idx + (int64_t)unit * k_max;
 
     // The first batch of scores is requested before the schedule lookup is resolved.
@@ -365,7 +352,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
         return;
     }
 
-    // Keys into LDS; block min and max.
+    // Keys into LDS; this thread's min and max of them.
     uint32_t kmin = 0xffffffffu, kmax = 0u;
     for (int base = 0; base < n; base += kTopkThreads * kTopkBatch) {
         if (base > 0) {
@@ -388,136 +375,8 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(
             }
         }
     }
-    for (int t = tid; t < 256; t += kTopkThreads)
-        hist[0][t] = 0u;
-    kmin = wave_min(kmin);
-    kmax = wave_max(kmax);
-    if (lane == 0) {
-        red_a[wave] = kmin;
-        red_b[wave] = kmax;
-    }
-    __syncthreads();
-    kmin = red_a[0];
-    kmax = red_b[0];
-#pragma unroll
-    for (int w = 1; w < kTopkWaves; ++w) {
-        kmin = min(kmin, red_a[w]);
-        kmax = max(kmax, red_b[w]);
-    }
-
-    // Radix select of the k-th largest key, 8-bit digits from the highest bit where the
-    // keys differ down (the bits above it are common to all keys).  After each digit the
-    // candidates are the keys whose bits >= lo equal `prefix`; `rem` of them are still to be
-    // taken.  When the chosen bin holds exactly `rem` keys every candidate is taken and the
-    // selection is "bits >= lo at least prefix", with no tie left to break.
-    uint32_t prefix = kmax;
-    uint32_t rem = (uint32_t)k;
-    bool exact = true;  // false: stopped early, keep keys >= prefix (bits below lo zero)
-    int lo = 0;
-    if (kmin != kmax) {
-        int hi = 31 - __builtin_clz(kmin ^ kmax);
-        int cur = 0;
-        while (hi >= 0) {
-            lo = hi >= 7 ? hi - 7 : 0;
-            const uint32_t width_mask = (1u << (hi - lo + 1)) - 1u;
-            const uint32_t above = hi >= 31 ? 0u : (0xffffffffu << (hi + 1));
-            const uint32_t want = prefix & above;
-            for (int base = 0; base < n; base += kTopkThreads * 4) {
-                uint32_t kv[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int i = base + tid + kTopkThreads * j;
-                    kv[j] = i < n ? keys[i] : 0u;
-                }
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (base + tid + kTopkThreads * j < n && (kv[j] & above) == want)
-                        atomicAdd(&hist[cur][(kv[j] >> lo) & width_mask], 1u);
-            }
-            for (int t = tid; t < 256; t += kTopkThreads)
-                hist[cur ^ 1][t] = 0u;  // ready for the next digit
-            __syncthreads();
-            if (wave == 0) {
-                // lane l owns digits 255-4l .. 252-4l; counts accumulate from the top down
-                const uint32_t c0 = hist[cur][255 - 4 * lane], c1 = hist[cur][254 - 4 * lane];
-                const uint32_t c2 = hist[cur][253 - 4 * lane], c3 = hist[cur][252 - 4 * lane];
-                const uint32_t tot = c0 + c1 + c2 + c3;
-                const uint32_t incl = wave_scan_add(tot);
-                uint32_t acc = incl - tot;  // keys with a larger digit
-                if (acc < rem && rem <= incl) {
-                    int d;
-                    uint32_t cnt;
-                    if (rem <= acc + c0) {
-                        d = 255 - 4 * lane;
-                        cnt = c0;
-                    } else if (rem <= acc + c0 + c1) {
-                        acc += c0;
-                        d = 254 - 4 * lane;
-                        cnt = c1;
-                    } else if (rem <= acc + c0 + c1 + c2) {
-                        acc += c0 + c1;
-                        d = 253 - 4 * lane;
-                        cnt = c2;
-                    } else {
-                        acc += c0 + c1 + c2;
-                        d = 252 - 4 * lane;
-                        cnt = c3;
-                    }
-                    s_digit = (uint32_t)d;
-                    s_rem = rem - acc;
-                    s_done = cnt == rem - acc;
-                }
-            }
-            __syncthreads();
-            prefix = want | (s_digit << lo);
-            rem = s_rem;
-            if (s_done) {
-                exact = false;
-                break;
-            }
-            hi = lo - 1;
-            cur ^= 1;
-        }
-    }
-    // Selection rule as "key > T" plus the first `rem` keys equal to T in page order.
-    uint32_t T = prefix;
-    if (!exact) {
-        T = prefix - 1u;  // keys >= prefix (prefix > 0 here, as fewer than n keys are kept)
-        rem = 0u;
-    }
-
-    // Ranks: a kept page's position is (#keys > T before it) + min(#keys == T before it, rem).
-    const int seg = (n + kTopkThreads - 1) / kTopkThreads;
-    const int s0 = min(n, tid * seg);
-    const int s1 = min(n, s0 + seg);
-    uint32_t gt = 0u, eq = 0u;
-    for (int i = s0; i < s1; ++i) {
-        const uint32_t key = keys[i];
-        gt += key > T;
-        eq += key == T;
-    }
-    const uint32_t packed = (gt << 16) | eq;  // n <= 15360 < 2^16
-    uint32_t incl = wave_scan_add(packed);
-    if (lane == 63)
-        red_c[wave] = incl;
-    __syncthreads();
-    uint32_t before = incl - packed;
-    for (int w = 0; w < wave; ++w)
-        before += red_c[w];
-    uint32_t gt_b = before >> 16, eq_b = before & 0xffffu;
-    for (int i = s0; i < s1; ++i) {
-        const uint32_t key = keys[i];
-        if (key > T) {
-            const uint32_t pos = gt_b + min(eq_b, rem);
-            if (pos < (uint32_t)k)
-                row[pos] = i;
-            ++gt_b;
-        } else if (key == T) {
-            if (eq_b < rem && gt_b + eq_b < (uint32_t)k)
-                row[gt_b + eq_b] = i;
-            ++eq_b;
-        }
-    }
+    block_topk<kTopkThreads>(keys, n, k, kmin, kmax, t,
+                             [&](uint32_t pos, int i) { row[pos] = i; });
     for (int i = k + tid; i < k_max; i += kTopkThreads)
         row[i] = -1;
 }
@@ -529,14 +388,11 @@ size_t score_topk_workspace(const sparrow_shape_t &s)
     return (size_t)s.batch * s.num_kv_heads * s.max_pages_per_seq * sizeof(float);
 }
 
-hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta,
+hipError_t launch_page_score(const sparrow_shape_t &s, const void *q, void *meta,
                              const int32_t *block_table, const int32_t *seq_lens,
-                             const Sched &sched, int32_t k_max, int32_t *out_k,
-                             int32_t *out_idx, void *workspace, const AppendArgs &app,
-                             hipStream_t stream)
+                             const Sched &sched, int32_t k_max, float *scores,
+                             const AppendArgs &app, hipStream_t stream)
 {
-    float *scores = static_cast<float *>(workspace);
-    const int units = s.batch * s.num_kv_heads;
     const int zs = (s.num_kv_heads + kScoreHeads - 1) / kScoreHeads;
     // A grid of fewer 32-page workgroups than compute units (a small batch: the step is
     // latency-bound) takes 8-page workgroups instead, so that a wave scores one batch and
@@ -559,9 +415,14 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta
                        static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(meta),
                        block_table, seq_lens, sched, k_max, s.num_q_heads, s.num_kv_heads,
                        s.page_size, s.max_pages_per_seq, s.num_phys_pages, scores, app);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
+    return hipGetLastError();
+}
+
+hipError_t launch_topk(const sparrow_shape_t &s, const int32_t *seq_lens, const Sched &sched,
+                       int32_t k_max, const float *scores, int32_t *out_k, int32_t *out_idx,
+                       hipStream_t stream)
+{
+    const int units = s.batch * s.num_kv_heads;
     // Many units: smaller workgroups, so more of them share a CU (the per-unit work is
     // latency-bound); few units: larger ones, so each finishes sooner.
     const bool many = units >= kTopkManyUnits;
@@ -570,6 +431,20 @@ hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta
                        sched, k_max, s.num_kv_heads, s.page_size, s.max_pages_per_seq, out_k,
                        out_idx);
     return hipGetLastError();
+}
+
+hipError_t launch_score_topk(const sparrow_shape_t &s, const void *q, void *meta,
+                             const int32_t *block_table, const int32_t *seq_lens,
+                             const Sched &sched, int32_t k_max, int32_t *out_k,
+                             int32_t *out_idx, void *workspace, const AppendArgs &app,
+                             hipStream_t stream)
+{
+    float *scores = static_cast<float *>(workspace);
+    const hipError_t e = launch_page_score(s, q, meta, block_table, seq_lens, sched, k_max,
+                                           scores, app, stream);
+    if (e != hipSuccess)
+        return e;
+    return launch_topk(s, seq_lens, sched, k_max, scores, out_k, out_idx, stream);
 }
 
 }  // namespace sparrow

@@ -38,13 +38,14 @@ SPARROW_LOGITS_BF16 = 1
 SPARROW_OP_SCORE_TOPK = 0
 SPARROW_OP_SPARSE_ATTN = 1
 SPARROW_OP_DENSE_ATTN = 2
+SPARROW_OP_DECODE_STEP = 3
 SPARROW_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 EXPORTS = ("sparrow_page_meta_update", "sparrow_append_kv", "sparrow_page_score_topk",
            "sparrow_append_score_topk", "sparrow_sparse_decode_attn", "sparrow_dense_decode_attn",
            "sparrow_acceptance_rate", "sparrow_acceptance_rate_topk", "sparrow_tail_stats",
-           "sparrow_stream_read", "sparrow_sparse_decode_attn_noalloc", "sparrow_budget_bound",
-           "sparrow_workspace_size", "sparrow_status_string")
+           "sparrow_stream_read", "sparrow_sparse_decode_attn_noalloc", "sparrow_decode_step",
+           "sparrow_budget_bound", "sparrow_workspace_size", "sparrow_status_string")
 
 
 class SparrowError(RuntimeError):
@@ -101,7 +102,10 @@ def load():
     lib.sparrow_stream_read.argtypes = [_p, ctypes.c_int64, _p, _p]
     lib.sparrow_sparse_decode_attn_noalloc.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _i32,
                                                        ctypes.c_float, _p, _i32, _p]
-    for fn in EXPORTS[:11]:
+    lib.sparrow_decode_step.argtypes = [sp, _p, _p, _p, _p, _p, _p, _p, _p,
+                                        ctypes.POINTER(Schedule), _i32, ctypes.c_float, _p, _p,
+                                        _p, _i32, _p, ctypes.c_size_t, _p]
+    for fn in EXPORTS[:12]:
         getattr(lib, fn).restype = ctypes.c_int
     lib.sparrow_budget_bound.argtypes = [_p, ctypes.c_int64, _i32, _i32, _i32, _p, _p, _i32, _p]
     lib.sparrow_budget_bound.restype = ctypes.c_int32
@@ -152,6 +156,15 @@ def sparrow_sparse_decode_attn_noalloc(shape, q, k_cache, v_cache, block_table, 
     return load().sparrow_sparse_decode_attn_noalloc(ctypes.byref(shape), q, k_cache, v_cache,
                                                      block_table, seq_lens, k, idx, k_max, scale,
                                                      out, out_dtype, stream)
+
+
+def sparrow_decode_step(shape, q, k_new, v_new, k_cache, v_cache, meta, block_table, seq_lens,
+                        schedule, k_max, scale, out_k, out_idx, out, out_dtype, workspace,
+                        ws_bytes, stream):
+    return load().sparrow_decode_step(ctypes.byref(shape), q, k_new, v_new, k_cache, v_cache,
+                                      meta, block_table, seq_lens, ctypes.byref(schedule), k_max,
+                                      scale, out_k, out_idx, out, out_dtype, workspace, ws_bytes,
+                                      stream)
 
 
 def sparrow_dense_decode_attn(shape, q, k_cache, v_cache, block_table, seq_lens, scale, out,
@@ -455,6 +468,7 @@ class SparseDecodeStep:
                                                           SPARROW_OP_SCORE_TOPK), dev)
         self.ws_attn = _workspace(sparrow_workspace_size(self.shape, self.k_max,
                                                          SPARROW_OP_SPARSE_ATTN), dev)
+        self._ws_step = None
 
     # Every method takes an optional ``seq_lens`` tensor that replaces the one given at
     # construction for that call (a decode loop advances the lengths step by step).
@@ -492,6 +506,21 @@ class SparseDecodeStep:
             _ptr(self.block_table), self._lens(seq_lens), _ptr(self.k), _ptr(self.idx),
             self.k_max, self.scale, _ptr(self.out), SPARROW_OUT_F32, _ptr(self.ws_attn),
             self.ws_attn.numel(), stream))
+
+    def decode_step(self, k_new, v_new, stream, seq_lens=None):
+        """The whole step in one call (sparrow_decode_step): append the decoded token
+        (k_new/v_new [B][Hkv][D], or both None for no append), select pages, attend; the
+        same results as append_score_topk (or score_topk) followed by attend."""
+        if self._ws_step is None:
+            self._ws_step = _workspace(sparrow_workspace_size(self.shape, self.k_max,
+                                                              SPARROW_OP_DECODE_STEP),
+                                       self.q.device)
+        _check("sparrow_decode_step", sparrow_decode_step(
+            self.shape, _ptr(self.q), _ptr(k_new), _ptr(v_new), _ptr(self.k_cache),
+            _ptr(self.v_cache), _ptr(self.meta), _ptr(self.block_table), self._lens(seq_lens),
+            self.sched, self.k_max, self.scale, _ptr(self.k), _ptr(self.idx), _ptr(self.out),
+            SPARROW_OUT_F32, _ptr(self._ws_step), self._ws_step.numel(), stream))
+        return self.out
 
     def run(self, first_pos=None, stream=None):
         stream = _stream(self.q.device) if stream is None else stream

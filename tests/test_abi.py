@@ -113,13 +113,21 @@ def call(fn, shape, **over):
         return S.sparrow_sparse_decode_attn(shape, a["q"], a["k"], a["v"], a["bt"], a["lens"],
                                             a["kk"], a["idx"], a["k_max"], 0.088, a["out"],
                                             a["dtype"], ws, ws_bytes, None)
+    if fn == "step":
+        a = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k=FAKE, v=FAKE, meta=FAKE, bt=FAKE, lens=FAKE,
+                 sched=sched(), k_max=8, out_k=FAKE, out_idx=FAKE, out=FAKE, dtype=0)
+        a.update(over)
+        return S.sparrow_decode_step(shape, a["q"], a["k_new"], a["v_new"], a["k"], a["v"],
+                                     a["meta"], a["bt"], a["lens"], a["sched"], a["k_max"], 0.088,
+                                     a["out_k"], a["out_idx"], a["out"], a["dtype"], ws, ws_bytes,
+                                     None)
     a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, dtype=0)
     a.update(over)
     return S.sparrow_dense_decode_attn(shape, a["q"], a["k"], a["v"], a["bt"], a["lens"], 0.088,
                                        a["out"], a["dtype"], ws, ws_bytes, None)
 
 
-@pytest.mark.parametrize("fn", ["meta", "append", "topk", "fused", "sparse", "dense"])
+@pytest.mark.parametrize("fn", ["meta", "append", "topk", "fused", "sparse", "dense", "step"])
 @pytest.mark.parametrize("bad,status", BAD_SHAPES)
 def test_bad_shapes_are_rejected(lib, fn, bad, status):
     bad = dict(bad)
@@ -136,6 +144,8 @@ NULLS = {
     "fused": ["q", "k_new", "v_new", "k", "v", "meta", "bt", "lens", "out_k", "out_idx"],
     "sparse": ["q", "k", "v", "bt", "lens", "kk", "idx", "out"],
     "dense": ["q", "k", "v", "bt", "lens", "out"],
+    # (k_new and v_new may both be NULL: no append; one of them alone is refused below)
+    "step": ["q", "k", "v", "meta", "bt", "lens", "out_k", "out_idx", "out"],
 }
 
 
@@ -159,9 +169,16 @@ def test_null_shape_and_schedule_are_rejected(lib):
     assert call("fused", good_shape(), sched=S.Schedule(2048, 1, FAKE, None, 10)) == \
         S.SPARROW_EINVAL
     assert call("sparse", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    assert call("step", good_shape(), k_max=0) == S.SPARROW_EINVAL
+    assert call("step", good_shape(), sched=S.Schedule(2048, 1, FAKE, FAKE, 10, 0, -1)) == \
+        S.SPARROW_EINVAL
+    assert call("step", good_shape(), sched=S.Schedule(2048, 1, None, FAKE, 10)) == \
+        S.SPARROW_EINVAL
+    assert call("step", good_shape(), k_new=None) == S.SPARROW_EINVAL
+    assert call("step", good_shape(), v_new=None) == S.SPARROW_EINVAL
     # no budget exceeds the largest page count, so a longer row is refused
     big = S.SPARROW_MAX_PAGES_PER_SEQ + 1
-    for fn in ("topk", "fused", "sparse"):
+    for fn in ("topk", "fused", "sparse", "step"):
         assert call(fn, good_shape(), k_max=big) == S.SPARROW_EINVAL
         assert call(fn, good_shape(), k_max=2**31 - 1) == S.SPARROW_EINVAL
     assert call("topk", good_shape(), k_max=S.SPARROW_MAX_PAGES_PER_SEQ, ws_bytes=0) == \
@@ -171,12 +188,14 @@ def test_null_shape_and_schedule_are_rejected(lib):
 def test_unsupported_output_dtype(lib):
     assert call("sparse", good_shape(), dtype=2) == S.SPARROW_EUNSUPPORTED
     assert call("dense", good_shape(), dtype=7) == S.SPARROW_EUNSUPPORTED
+    assert call("step", good_shape(), dtype=2) == S.SPARROW_EUNSUPPORTED
 
 
 @pytest.mark.parametrize("fn,op", [("topk", S.SPARROW_OP_SCORE_TOPK),
                                    ("fused", S.SPARROW_OP_SCORE_TOPK),
                                    ("sparse", S.SPARROW_OP_SPARSE_ATTN),
-                                   ("dense", S.SPARROW_OP_DENSE_ATTN)])
+                                   ("dense", S.SPARROW_OP_DENSE_ATTN),
+                                   ("step", S.SPARROW_OP_DECODE_STEP)])
 def test_workspace_checks(lib, fn, op):
     shape = good_shape()
     need = S.sparrow_workspace_size(shape, 8, op)
@@ -187,7 +206,7 @@ def test_workspace_checks(lib, fn, op):
 
 def test_empty_batch_enqueues_nothing(lib):
     shape = good_shape(batch=0)
-    for fn in ("meta", "append", "topk", "fused", "sparse", "dense"):
+    for fn in ("meta", "append", "topk", "fused", "sparse", "dense", "step"):
         assert call(fn, shape, ws=None, ws_bytes=0) == S.SPARROW_OK
 
 
@@ -202,6 +221,11 @@ def test_workspace_size_properties(lib):
     b = S.sparrow_workspace_size(shape, 64, S.SPARROW_OP_SPARSE_ATTN)
     assert 0 < a <= b
     assert S.sparrow_workspace_size(shape, 1, S.SPARROW_OP_SCORE_TOPK) == 4 * 8 * 64 * 4
+    # the whole step: the scores (rounded up to 256 bytes), then the attention's workspace
+    score = S.sparrow_workspace_size(shape, 8, S.SPARROW_OP_SCORE_TOPK)
+    assert S.sparrow_workspace_size(shape, 8, S.SPARROW_OP_DECODE_STEP) == \
+        (score + 255) // 256 * 256 + a
+    assert S.sparrow_workspace_size(shape, 0, S.SPARROW_OP_DECODE_STEP) == 0
 
 
 def test_status_strings(lib):
@@ -288,7 +312,8 @@ def test_tensor_wrappers_refuse_host_tensors():
 
 VEC16 = {"meta": ["k_cache", "meta"], "append": ["k_new", "v_new", "k", "v", "meta"],
          "topk": ["q", "meta", "ws"], "fused": ["q", "k_new", "v_new", "k", "v", "meta", "ws"],
-         "sparse": ["q", "k", "v", "out", "ws"], "dense": ["q", "k", "v", "out", "ws"]}
+         "sparse": ["q", "k", "v", "out", "ws"], "dense": ["q", "k", "v", "out", "ws"],
+         "step": ["q", "k_new", "v_new", "k", "v", "meta", "out", "ws"]}
 
 
 @pytest.mark.parametrize("fn,arg", [(f, a) for f, args in NULLS.items() for a in args] +
