@@ -247,8 +247,9 @@ int sparrow_append_score_topk(const sparrow_shape_t *shape, const void *q, const
  * computed with bf16 operands and fp32 accumulation (the softmax weights are
  * rounded to bf16 before they multiply V).  An empty token set gives a zero
  * row.  out_dtype is SPARROW_OUT_F32 or SPARROW_OUT_BF16.
- * The order of the fp32 sums depends only on the shape, k_max and the page
- * lists, so repeated calls give identical results.  A call with at most 256
+ * The order of the fp32 sums depends only on the shape, k_max, the page lists
+ * and the device (its count of resident waves), so repeated calls on one GPU
+ * give identical results.  A call with at most 256
  * (sequence, KV head) units, at most 8 query heads per KV head,
  * k_max * page_size <= 1024 and max_pages_per_seq <= 4096 runs one workgroup
  * per unit and leaves the workspace untouched; larger calls split the lists
