@@ -1,7 +1,8 @@
 """A decode step captured in a HIP graph (through torch's graph capture) replays to the
 same results as the eager calls.  The library records no memset or allocation, so the
 captured kernels are the whole step: several layers, each an append fused with scoring
-and top-k, then sparse attention."""
+and top-k, then sparse attention - or each one sparrow_decode_step call, on layers that
+take the one-kernel selection and attention and layers that stream."""
 import numpy as np
 import pytest
 import torch
@@ -22,8 +23,8 @@ def _need_gpu(gpu_device):
     yield
 
 
-def make_layer(seed):
-    w = W.small(B=3, Hq=8, Hkv=2, ps=16, lengths=(300, 1000, 17), seed=seed,
+def make_layer(seed, G=4):
+    w = W.small(B=3, Hq=2 * G, Hkv=2, ps=16, lengths=(300, 1000, 17), seed=seed,
                 schedule=W.fraction_budget(1, 5, floor_pages=2), hot_pages=2)
     inp = W.generate(w, DEV, lengths=[300, 1000, 17])
     s = w.schedule
@@ -40,16 +41,22 @@ def make_layer(seed):
     return step, kn, vn
 
 
-def run_layers(layers, stream):
+def run_layers(layers, stream, whole):
     for step, kn, vn in layers:
-        step.append_score_topk(kn, vn, stream)
-        step.attend(stream)
+        if whole:
+            step.decode_step(kn, vn, stream)
+        else:
+            step.append_score_topk(kn, vn, stream)
+            step.attend(stream)
 
 
-def test_multi_layer_step_graph_replays_match_eager():
-    log("case graph replay, 4 layers")
-    layers = [make_layer(80 + i) for i in range(4)]
-    run_layers(layers, torch.cuda.current_stream().cuda_stream)
+@pytest.mark.parametrize("whole", [False, True])
+def test_multi_layer_step_graph_replays_match_eager(whole):
+    log(f"case graph replay, 4 layers, whole-step call {whole}")
+    # group sizes 4 and 10: the whole-step call selects and attends in one kernel on the
+    # first, streams on the second (more than 8 query heads per KV head)
+    layers = [make_layer(80 + i, G=4 if i % 2 == 0 else 10) for i in range(4)]
+    run_layers(layers, torch.cuda.current_stream().cuda_stream, whole)
     torch.cuda.synchronize()
     eager = [(st.idx.clone(), st.k.clone(), st.out.clone(), st.meta.clone()) for st, _, _ in layers]
     graph = torch.cuda.CUDAGraph()
@@ -57,7 +64,7 @@ def test_multi_layer_step_graph_replays_match_eager():
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
         with torch.cuda.graph(graph, stream=side):
-            run_layers(layers, torch.cuda.current_stream().cuda_stream)
+            run_layers(layers, torch.cuda.current_stream().cuda_stream, whole)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     for rep in range(3):
