@@ -468,7 +468,10 @@ class SparseDecodeStep:
                                                           SPARROW_OP_SCORE_TOPK), dev)
         self.ws_attn = _workspace(sparrow_workspace_size(self.shape, self.k_max,
                                                          SPARROW_OP_SPARSE_ATTN), dev)
-        self._ws_step = None
+        # allocated here, not on first use, so that a first call under graph capture
+        # allocates nothing
+        self.ws_step = _workspace(sparrow_workspace_size(self.shape, self.k_max,
+                                                         SPARROW_OP_DECODE_STEP), dev)
 
     # Every method takes an optional ``seq_lens`` tensor that replaces the one given at
     # construction for that call (a decode loop advances the lengths step by step).
@@ -511,15 +514,11 @@ class SparseDecodeStep:
         """The whole step in one call (sparrow_decode_step): append the decoded token
         (k_new/v_new [B][Hkv][D], or both None for no append), select pages, attend; the
         same results as append_score_topk (or score_topk) followed by attend."""
-        if self._ws_step is None:
-            self._ws_step = _workspace(sparrow_workspace_size(self.shape, self.k_max,
-                                                              SPARROW_OP_DECODE_STEP),
-                                       self.q.device)
         _check("sparrow_decode_step", sparrow_decode_step(
             self.shape, _ptr(self.q), _ptr(k_new), _ptr(v_new), _ptr(self.k_cache),
             _ptr(self.v_cache), _ptr(self.meta), _ptr(self.block_table), self._lens(seq_lens),
             self.sched, self.k_max, self.scale, _ptr(self.k), _ptr(self.idx), _ptr(self.out),
-            SPARROW_OUT_F32, _ptr(self._ws_step), self._ws_step.numel(), stream))
+            SPARROW_OUT_F32, _ptr(self.ws_step), self.ws_step.numel(), stream))
         return self.out
 
     def run(self, first_pos=None, stream=None):
