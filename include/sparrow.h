@@ -18,7 +18,8 @@
  *                                 cost model, Eq. sparse-cost),
  *   4. sparrow_dense_decode_attn  the dense paged decode it is measured against
  *                                 (Eq. dense-cost).
- *   sparrow_append_score_topk fuses the append into step 2.
+ *   sparrow_append_score_topk fuses the append into step 2, and
+ *   sparrow_decode_step runs the append and steps 2 and 3 in one call.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -305,7 +306,7 @@ int sparrow_sparse_decode_attn_noalloc(const sparrow_shape_t *shape, const void 
  * calls in sequence bit for bit.  When the attention call would run one
  * workgroup per unit (see sparrow_sparse_decode_attn), the budget, the top-k
  * and the attention run in one kernel after the scoring kernel, with the
- * selection kept on chip: two launches instead of four.
+ * selection kept on chip: two launches instead of three.
  *
  * Arguments: those of the two calls (k_new and v_new both NULL or both set);
  * workspace of at least sparrow_workspace_size(shape, k_max,

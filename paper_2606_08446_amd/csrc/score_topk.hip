@@ -16,7 +16,9 @@
 // order-preserving uint32 keys in LDS; a radix select over 8-bit digits (from the highest
 // bit where the keys differ, stopping as soon as the selection is decided) finds the
 // threshold T and how many keys equal to T to keep; one block scan of (count > T,
-// count == T) then places every kept page at its rank in ascending page order.
+// count == T) then places every kept page at its rank in ascending page order.  That
+// select-and-rank core is block_topk (topk.h), shared with the attention kernel that selects
+// and attends in one workgroup for small problems.
 #include "common.h"
 #include "topk.h"
 #include "wave.h"
