@@ -270,3 +270,39 @@ def test_step_full_size(cfg):
                            s.frac_den)
     assert not unit_path(inp, k_max)
     same_step(inp, meta, kn, vn, k_max)
+
+
+@pytest.mark.parametrize("case", [0, 3, 6])
+def test_step_sequence_past_the_block_table(case):
+    """The longest sequence gets a length one past what its block table addresses: the
+    append leaves it alone and its length is clamped, in both forms of the step."""
+    G, Hkv, ps, lengths, sched, _ = CASES[case]
+    log(f"case decode step {case}, a sequence past its block table")
+    inp, meta, _, kn, vn = append_case(G, Hkv, ps, lengths, seed=590 + case, schedule=sched,
+                                       skip_last=True)
+    s = inp.workload.schedule
+    k_max = S.budget_bound(np.minimum(inp.lens_host, ps * inp.max_pages), ps, s.bin_tokens,
+                           s.min_pages, s.frac_num, s.frac_den)
+    same_step(inp, meta, kn, vn, k_max)
+
+
+@pytest.mark.parametrize("case", [0, 6])
+def test_step_absent_pages(case):
+    """Block-table entries outside the cache inside the sequences (absent pages: scored 0,
+    left out of the attention, no append to them) give the same results in both forms."""
+    G, Hkv, ps, lengths, sched, _ = CASES[case]
+    log(f"case decode step {case}, absent pages")
+    inp, meta, _, kn, vn = append_case(G, Hkv, ps, lengths, seed=600 + case, schedule=sched,
+                                       skip_last=False)
+    bt = inp.block_table.clone()
+    P = inp.num_phys_pages
+    for b, L in enumerate(lengths):
+        n = (L + ps - 1) // ps
+        if n >= 3:
+            bt[b, 1] = P + 3          # past the cache
+            bt[b, n - 1] = -2         # negative: the page that takes the appended token
+    inp.block_table.copy_(bt)
+    s = inp.workload.schedule
+    k_max = S.budget_bound(inp.lens_host, ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den)
+    same_step(inp, meta, kn, vn, k_max)
