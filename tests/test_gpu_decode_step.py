@@ -306,3 +306,52 @@ def test_step_absent_pages(case):
     k_max = S.budget_bound(inp.lens_host, ps, s.bin_tokens, s.min_pages, s.frac_num,
                            s.frac_den)
     same_step(inp, meta, kn, vn, k_max)
+
+
+def random_step_case(seed):
+    """A seeded shape for the whole-step call: two seeds in three are drawn inside the
+    one-kernel selection and attention's limits (G <= 8, a fixed budget with
+    k_max * page_size <= 1024, few units), the third from any shape and schedule form."""
+    rng = np.random.default_rng(4200 + seed)
+    small = seed % 3 != 2
+    G = int(rng.choice([1, 2, 3, 4, 5, 8] if small else [1, 2, 4, 8, 12, 16]))
+    Hkv = int(rng.integers(1, 9 if small else 13))
+    ps = int(rng.choice([16, 32, 64, 128]))
+    B = int(rng.integers(1, 7))
+    lengths = [int(x) for x in rng.integers(0, 9000, size=B)]
+    if rng.random() < 0.4:
+        lengths[int(rng.integers(0, B))] = int(rng.choice([0, 1, ps, ps + 1]))
+    if small:
+        sched = W.fixed_budget(int(rng.integers(1, 1024 // ps + 1)))
+    elif rng.random() < 0.5:
+        sched = W.fraction_budget(int(rng.integers(1, 5)), int(rng.integers(5, 20)),
+                                  floor_pages=int(rng.integers(0, 6)))
+    else:
+        sched = W.rising_permille(2048, 2048, 8192, int(rng.integers(20, 100)),
+                                  int(rng.integers(100, 400)))
+    return G, Hkv, ps, tuple(lengths), sched
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shapes_whole_step(seed):
+    """Seeded random shapes: the whole-step call equals the separate calls bit for bit, and
+    its budgets, page lists and outputs match the CPU oracle's step after the append."""
+    G, Hkv, ps, lengths, sched = random_step_case(seed)
+    inp, meta, meta0, kn, vn = append_case(G, Hkv, ps, lengths, seed=610 + seed,
+                                           schedule=sched, skip_last=False)
+    s = inp.workload.schedule
+    k_max = S.budget_bound(inp.lens_host, ps, s.bin_tokens, s.min_pages, s.frac_num,
+                           s.frac_den)
+    log(f"case decode step random {seed}: G={G} Hkv={Hkv} ps={ps} lens={lengths} "
+        f"k_max {k_max}, unit path {unit_path(inp, k_max)}")
+    h = host(inp)
+    (k, idx, out), _ = same_step(inp, meta, kn, vn, k_max)
+    kc, vc, _ = oracle.append_kv(W.bf16_bits(kn), W.bf16_bits(vn), h["k"], h["v"], h["bt"],
+                                 h["lens"], meta0)
+    ref = oracle.sparse_step(h["q"], kc, vc, h["bt"], h["lens"],
+                             (s.bin_tokens, s.min_pages, s.frac_num, s.frac_den), k_max, SCALE)
+    k_h, idx_h = k.cpu().numpy(), idx.cpu().numpy()
+    check_indices(k_h, idx_h, ref["k"], ref["idx"], ref["scores32"], ref["scores64"],
+                  h["lens"], ps, k_max)
+    ref_out = oracle.attention(h["q"], kc, vc, h["bt"], h["lens"], SCALE, k_h, idx_h)
+    check_out(out.cpu().numpy().astype(np.float64), ref_out, f"decode step random {seed}")
