@@ -2,13 +2,14 @@
 // Eq. 1 of arXiv 2606.08446) and its lower-tail statistic per length bin (Sec. 3.1-3.2).
 //
 // k_acceptance: alpha_t = sum_x min(p(x), q(x)) with p, q the softmax of the target and draft
-// logit rows at inverse temperature tau.  One 1024-thread workgroup per token makes two
-// passes over its two rows: an online log-sum-exp of both (plain loads), then
+// logit rows at inverse temperature tau.  One 1024-thread workgroup per token (one per CU)
+// makes two passes over its two rows: an online log-sum-exp of both (plain loads), then
 // sum_x exp(min(tau a_x - P, tau b_x - Q)) - one exp per vocabulary entry, since
-// min(e^u, e^v) = e^min(u, v) - with non-temporal loads, from the end of the rows back, so
-// the part read last in the first pass is read first again while the L2 may still hold
-// it.  The launch reserves LDS for one workgroup per CU, which keeps the rows in flight
-// (and so the traffic between the two reads of an element) small.
+// min(e^u, e^v) = e^min(u, v).  The first vectors of the rows stay on chip between the
+// passes, 128 KiB of them in LDS and 12 (fp32) or 10 (bf16) per thread and row in registers
+// (43 % of an fp32 row pair of Qwen3's vocabulary, three quarters of a bf16 one); the
+// rest is read again, with non-temporal loads and from the end of the rows back, so the
+// part read last in the first pass is read first again while the L2 may still hold it.
 // Rows are read as 16-byte vectors; a row that does not start 16-byte aligned is handled
 // with scalar head and tail elements.  Accumulation is fp32 per thread, tree reductions
 // across the workgroup.
@@ -28,12 +29,15 @@ namespace {
 
 constexpr int kAccThreads = 1024;
 constexpr int kAccWaves = kAccThreads / 64;
+constexpr int kAccLdsVecs = 4;  // 16-byte vectors of each row a thread keeps in LDS
 constexpr int kTailThreads = 1024;
 constexpr int kTailWaves = kTailThreads / 64;
 
 template <typename T> struct Logit;
 template <> struct Logit<float> {
     static constexpr int kVec = 4;  // elements per 16-byte vector
+    static constexpr int kKeep = 12;  // vectors of each row a thread keeps in registers
+    static constexpr int kBatch = 1;  // vectors of each row per load batch of either pass
     __device__ static float at(const float *row, int64_t i) { return row[i]; }
     __device__ static void unpack(u32x4_t v, float (&x)[kVec])
     {
@@ -44,6 +48,8 @@ template <> struct Logit<float> {
 };
 template <> struct Logit<uint16_t> {
     static constexpr int kVec = 8;
+    static constexpr int kKeep = 10;  // (measured: the fastest pairs that compile without
+    static constexpr int kBatch = 2;  // spills)
     __device__ static float at(const uint16_t *row, int64_t i)
     {
         return __uint_as_float((uint32_t)row[i] << 16);
@@ -144,22 +150,62 @@ __device__ __forceinline__ float oriented(float x)
 }
 
 template <typename T, bool kNeg>
+__device__ __forceinline__ void lse_add_vec(Lse &a, Lse &b, u32x4_t va, u32x4_t vb, float ts)
+{
+    constexpr int W = Logit<T>::kVec;
+    float xa[W], xb[W];
+    Logit<T>::unpack(va, xa);
+    Logit<T>::unpack(vb, xb);
+#pragma unroll
+    for (int e = 0; e < W; ++e) {
+        xa[e] = oriented<kNeg>(xa[e]);
+        xb[e] = oriented<kNeg>(xb[e]);
+    }
+    lse_add(a, xa, ts);
+    lse_add(b, xb, ts);
+}
+
+// sum over the vector's entries of 2^min(ts a - P, ts b - Q)
+template <typename T, bool kNeg>
+__device__ __forceinline__ float min_sum_vec(u32x4_t va, u32x4_t vb, float ts, float P, float Q)
+{
+    constexpr int W = Logit<T>::kVec;
+    float xa[W], xb[W];
+    Logit<T>::unpack(va, xa);
+    Logit<T>::unpack(vb, xb);
+    float acc = 0.f;
+#pragma unroll
+    for (int e = 0; e < W; ++e)
+        acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(xa[e]), -P),
+                             fmaf(ts, oriented<kNeg>(xb[e]), -Q)));
+    return acc;
+}
+
+// The row pair's 16-byte vectors v = tid + j * kAccThreads: j < kAccLdsVecs stay in LDS
+// between the passes (s_keep, the thread's own slots), the next Logit<T>::kKeep in this
+// thread's registers, the rest are read again in the second pass.
+template <typename T, bool kNeg>
 __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict__ target,
                                                             const T *__restrict__ draft, int V,
                                                             float ts, float *__restrict__ alpha)
 {
+    extern __shared__ u32x4_t s_keep[];  // [2][kAccLdsVecs][kAccThreads]
     __shared__ Lse s_red[kAccWaves][2];
     __shared__ float s_sum[kAccWaves];
-    constexpr int W = Logit<T>::kVec;
+    constexpr int R = Logit<T>::kKeep, L = kAccLdsVecs, NB = Logit<T>::kBatch;
     const int64_t t = blockIdx.x;
     const T *pr = target + t * V;
     const T *qr = draft + t * V;
     const int tid = threadIdx.x;
     int head, nvec;
     row_split(pr, V, head, nvec);
-    const int tail0 = head + nvec * W;
+    const int tail0 = head + nvec * Logit<T>::kVec;
+    const u32x4_t *pv = reinterpret_cast<const u32x4_t *>(pr + head);
+    const u32x4_t *qv = reinterpret_cast<const u32x4_t *>(qr + head);
+    const int onchip = (R + L) * kAccThreads;  // vectors of each row held on chip
 
-    // ---- pass 1: log-sum-exp of both rows
+    // ---- pass 1: log-sum-exp of both rows (plain loads), keeping the first vectors: those
+    // for LDS first (their registers are free again before the kept ones are loaded)
     Lse a{-INFINITY, 0.f}, b{-INFINITY, 0.f};
     for (int i = tid; i < head; i += kAccThreads) {
         const float xa[1] = {oriented<kNeg>(Logit<T>::at(pr, i))};
@@ -173,48 +219,62 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
         lse_add(a, xa, ts);
         lse_add(b, xb, ts);
     }
-    const u32x4_t *pv = reinterpret_cast<const u32x4_t *>(pr + head);
-    const u32x4_t *qv = reinterpret_cast<const u32x4_t *>(qr + head);
-    int v = tid;
-    for (; v + 3 * kAccThreads < nvec; v += 4 * kAccThreads) {
-        u32x4_t ra[4], rb[4];
+    {
+        u32x4_t la[L], lb[L];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int j = 0; j < L; ++j) {
+            const int v = tid + j * kAccThreads;
+            la[j] = lb[j] = (u32x4_t){0u, 0u, 0u, 0u};
+            if (v < nvec) {
+                la[j] = pv[v];
+                lb[j] = qv[v];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < L; ++j) {
+            if (tid + j * kAccThreads < nvec) {
+                lse_add_vec<T, kNeg>(a, b, la[j], lb[j], ts);
+                s_keep[j * kAccThreads + tid] = la[j];
+                s_keep[(L + j) * kAccThreads + tid] = lb[j];
+            }
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the kept vectors' loads stay behind this point
+    u32x4_t ka[R], kb[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+        const int v = tid + (L + j) * kAccThreads;
+        ka[j] = kb[j] = (u32x4_t){0u, 0u, 0u, 0u};
+        if (v < nvec) {
+            ka[j] = pv[v];
+            kb[j] = qv[v];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < R; ++j)
+        if (tid + (L + j) * kAccThreads < nvec)
+            lse_add_vec<T, kNeg>(a, b, ka[j], kb[j], ts);
+    int v = onchip + tid;
+    for (; v + (NB - 1) * kAccThreads < nvec; v += NB * kAccThreads) {
+        u32x4_t ra[NB], rb[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
             ra[u] = pv[v + u * kAccThreads];
             rb[u] = qv[v + u * kAccThreads];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            float xa[W], xb[W];
-            Logit<T>::unpack(ra[u], xa);
-            Logit<T>::unpack(rb[u], xb);
-#pragma unroll
-            for (int e = 0; e < W; ++e) {
-                xa[e] = oriented<kNeg>(xa[e]);
-                xb[e] = oriented<kNeg>(xb[e]);
-            }
-            lse_add(a, xa, ts);
-            lse_add(b, xb, ts);
-        }
+        for (int u = 0; u < NB; ++u)
+            lse_add_vec<T, kNeg>(a, b, ra[u], rb[u], ts);
     }
-    for (; v < nvec; v += kAccThreads) {
-        float xa[W], xb[W];
-        Logit<T>::unpack(pv[v], xa);
-        Logit<T>::unpack(qv[v], xb);
-#pragma unroll
-        for (int e = 0; e < W; ++e) {
-            xa[e] = oriented<kNeg>(xa[e]);
-            xb[e] = oriented<kNeg>(xb[e]);
-        }
-        lse_add(a, xa, ts);
-        lse_add(b, xb, ts);
-    }
+    for (; v < nvec; v += kAccThreads)
+        lse_add_vec<T, kNeg>(a, b, pv[v], qv[v], ts);
     block_lse2(a, b, s_red);
     const float P = a.m + log2_hw(a.s);  // base-2 log-sum-exp of the scaled rows
     const float Q = b.m + log2_hw(b.s);
 
-    // ---- pass 2: sum of 2^min(ts a - P, ts b - Q) = exp(min(tau a - lse_a, tau b - lse_b)),
-    // vectors in reverse order
+    // ---- pass 2: sum of 2^min(ts a - P, ts b - Q) = exp(min(tau a - lse_a, tau b - lse_b)):
+    // the vectors read again first, from the end of the rows back (non-temporal loads), then
+    // those in LDS and in registers
     float acc = 0.f;
     for (int i = tid; i < head; i += kAccThreads)
         acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(Logit<T>::at(pr, i)), -P),
@@ -222,34 +282,36 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
     for (int i = tail0 + tid; i < V; i += kAccThreads)
         acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(Logit<T>::at(pr, i)), -P),
                              fmaf(ts, oriented<kNeg>(Logit<T>::at(qr, i)), -Q)));
-    v = tid;
-    for (; v + 3 * kAccThreads < nvec; v += 4 * kAccThreads) {
-        u32x4_t ra[4], rb[4];
+    const int nre = nvec - onchip;  // vectors read again (none if <= 0)
+    int w = tid;
+    for (; w + (NB - 1) * kAccThreads < nre; w += NB * kAccThreads) {
+        u32x4_t ra[NB], rb[NB];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            ra[u] = ld16_nt(pv + (nvec - 1 - (v + u * kAccThreads)));
-            rb[u] = ld16_nt(qv + (nvec - 1 - (v + u * kAccThreads)));
+        for (int u = 0; u < NB; ++u) {
+            ra[u] = ld16_nt(pv + (nvec - 1 - (w + u * kAccThreads)));
+            rb[u] = ld16_nt(qv + (nvec - 1 - (w + u * kAccThreads)));
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            float xa[W], xb[W];
-            Logit<T>::unpack(ra[u], xa);
-            Logit<T>::unpack(rb[u], xb);
-#pragma unroll
-            for (int e = 0; e < W; ++e)
-                acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(xa[e]), -P),
-                                     fmaf(ts, oriented<kNeg>(xb[e]), -Q)));
-        }
+        for (int u = 0; u < NB; ++u)
+            acc += min_sum_vec<T, kNeg>(ra[u], rb[u], ts, P, Q);
     }
-    for (; v < nvec; v += kAccThreads) {
-        float xa[W], xb[W];
-        Logit<T>::unpack(pv[nvec - 1 - v], xa);
-        Logit<T>::unpack(qv[nvec - 1 - v], xb);
+    for (; w < nre; w += kAccThreads)
+        acc += min_sum_vec<T, kNeg>(ld16_nt(pv + (nvec - 1 - w)), ld16_nt(qv + (nvec - 1 - w)),
+                                    ts, P, Q);
 #pragma unroll
-        for (int e = 0; e < W; ++e)
-            acc += exp2_hw(fminf(fmaf(ts, oriented<kNeg>(xa[e]), -P),
-                                 fmaf(ts, oriented<kNeg>(xb[e]), -Q)));
+    for (int j = 0; j < R; ++j) {
+        // (opaque to the compiler, so that it unpacks the kept vectors again here instead of
+        // holding the first pass's unpacked bf16 elements, twice the registers, until now)
+        if constexpr (sizeof(T) == 2)
+            asm volatile("" : "+v"(ka[j]), "+v"(kb[j]));
+        if (tid + (L + j) * kAccThreads < nvec)
+            acc += min_sum_vec<T, kNeg>(ka[j], kb[j], ts, P, Q);
     }
+#pragma unroll
+    for (int j = 0; j < L; ++j)
+        if (tid + j * kAccThreads < nvec)
+            acc += min_sum_vec<T, kNeg>(s_keep[j * kAccThreads + tid],
+                                        s_keep[(L + j) * kAccThreads + tid], ts, P, Q);
 #pragma unroll
     for (int x = 1; x < 64; x <<= 1)
         acc += __shfl_xor(acc, x, 64);
@@ -258,8 +320,8 @@ __global__ __launch_bounds__(kAccThreads) void k_acceptance(const T *__restrict_
     __syncthreads();
     if (tid == 0) {
         float total = 0.f;
-        for (int w = 0; w < kAccWaves; ++w)
-            total += s_sum[w];
+        for (int w2 = 0; w2 < kAccWaves; ++w2)
+            total += s_sum[w2];
         alpha[t] = total;
     }
 }
@@ -434,19 +496,19 @@ __global__ __launch_bounds__(kTailThreads) void k_tail_stats(
 hipError_t launch_acceptance(int64_t T, int V, int dtype, const void *target, const void *draft,
                              float tau, float *alpha, hipStream_t stream)
 {
-    // Unused dynamic LDS: with it only one workgroup fits on a CU.
-    constexpr size_t kOnePerCu = 96 * 1024;
+    // The vectors kept in LDS between the passes (128 KiB: one workgroup per CU).
+    constexpr size_t kKeep = 2 * (size_t)kAccLdsVecs * kAccThreads * sizeof(u32x4_t);
     const bool neg = tau < 0.f;
     const float ts = (neg ? -tau : tau) * 1.44269504088896340736f;  // |tau| log2(e)
     const dim3 grid((unsigned)T), block(kAccThreads);
     if (dtype == SPARROW_LOGITS_BF16) {
         auto k = neg ? k_acceptance<uint16_t, true> : k_acceptance<uint16_t, false>;
-        hipLaunchKernelGGL(k, grid, block, kOnePerCu, stream,
+        hipLaunchKernelGGL(k, grid, block, kKeep, stream,
                            static_cast<const uint16_t *>(target),
                            static_cast<const uint16_t *>(draft), V, ts, alpha);
     } else {
         auto k = neg ? k_acceptance<float, true> : k_acceptance<float, false>;
-        hipLaunchKernelGGL(k, grid, block, kOnePerCu, stream, static_cast<const float *>(target),
+        hipLaunchKernelGGL(k, grid, block, kKeep, stream, static_cast<const float *>(target),
                            static_cast<const float *>(draft), V, ts, alpha);
     }
     return hipGetLastError();

@@ -111,6 +111,38 @@ def test_acceptance_masked_entries(dtype, off):
         assert abs(g[2] - 1.0) <= 2e-6     # one finite entry in both rows: alpha = 1
 
 
+# Vocabulary sizes around the kernel's on-chip boundaries: each thread of the 1024 keeps the
+# first 4 16-byte vectors of each row in LDS and the next 12 (fp32) or 10 (bf16) in
+# registers between the two passes, and reads the rest again - so rows end just before and
+# just after 4096 and 16384 (fp32) or 14336 (bf16) vectors, and well past them.
+ONCHIP_V = {"f32": (16383, 16385, 65535, 65537, 80001),
+            "bf16": (32767, 32769, 114687, 114689, 130001)}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("vi", range(5))
+@pytest.mark.parametrize("off", [0, 1])
+def test_acceptance_around_the_on_chip_boundaries(dtype, vi, off):
+    V = ONCHIP_V[dtype][vi]
+    log(f"case acceptance on-chip boundary {dtype} V={V} offset={off}")
+    T = 4
+    li = W.generate_logits(W.small_logits(T=T + 1, V=V, seed=90 + vi, dtype=dtype), DEV)
+    t = li.target.view(-1)[off:off + T * V].view(T, V)
+    d = li.draft.view(-1)[off:off + T * V].view(T, V)
+    per_vec = 4 if dtype == "f32" else 8
+    edge = 4096 * per_vec
+    t[1, edge - 300:edge + 300] = float("-inf")   # a masked run across the LDS boundary
+    t[2, : V * 4 // 5] = float("-inf")             # most of both rows masked
+    d[2, : V * 4 // 5] = float("-inf")
+    for tau in (1.0, 0.6):
+        got = S.acceptance_rate(t, d, tau)
+        torch.cuda.synchronize()
+        ref = oracle.acceptance(host_rows(t), host_rows(d), tau)
+        err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+        log(f"  tau={tau} max abs err {err.max():.2e}")
+        assert err.max() <= ALPHA_TOL
+
+
 def test_acceptance_unaligned_row_starts():
     # views whose rows start off a 16-byte boundary (both rows in the same phase)
     li = W.generate_logits(W.small_logits(T=9, V=2051, seed=4), DEV)
