@@ -283,15 +283,86 @@ def _require_device(t):
         raise RuntimeError("libsparrow runs on the GPU only: tensors must be on a HIP device")
 
 
+def _expect(t, name, dtype, shape, device):
+    """Raise unless ``t`` is a contiguous tensor on ``device`` with exactly this dtype and shape.
+
+    The C ABI receives bare pointers: the kernels index every buffer with the sizes in the
+    shape struct, so a tensor of another dtype, shape or layout would be read or written
+    out of bounds.  The tensor-level wrappers check each buffer before any launch."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    _require_device(t)
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the other tensors on {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _expect_cache(q, k_cache, v_cache, block_table, seq_lens):
+    """q bf16 [B][Hq][D]; k_cache and v_cache bf16 [P][Hkv][ps][D]; block_table int32
+    [B][M]; seq_lens int32 [B].  Returns (B, Hq, Hkv, ps, D, P, M)."""
+    import torch
+    _require_device(q)
+    dev = q.device
+    if q.dim() != 3 or k_cache.dim() != 4 or block_table.dim() != 2:
+        raise ValueError("q must be [B][Hq][D], the caches [P][Hkv][ps][D], block_table [B][M]")
+    B, Hq, D = q.shape
+    P, Hkv, ps, _ = k_cache.shape
+    M = block_table.shape[1]
+    _expect(q, "q", torch.bfloat16, (B, Hq, D), dev)
+    _expect(k_cache, "k_cache", torch.bfloat16, (P, Hkv, ps, D), dev)
+    if v_cache is not None:
+        _expect(v_cache, "v_cache", torch.bfloat16, (P, Hkv, ps, D), dev)
+    _expect(block_table, "block_table", torch.int32, (B, M), dev)
+    _expect(seq_lens, "seq_lens", torch.int32, (B,), dev)
+    return B, Hq, Hkv, ps, D, P, M
+
+
+def _expect_meta(meta, P, Hkv, D, landmark, device):
+    import torch
+    if landmark == SPARROW_LANDMARK_MEAN:
+        _expect(meta, "meta", torch.float32, (P, Hkv, D), device)
+    else:
+        _expect(meta, "meta", torch.bfloat16, (P, Hkv, 2, D), device)
+
+
+def _expect_tables(min_pages, frac_num, device):
+    import torch
+    if min_pages.dim() != 1:
+        raise ValueError("min_pages must be a 1-D table")
+    _expect(min_pages, "min_pages", torch.int32, (min_pages.numel(),), device)
+    _expect(frac_num, "frac_num", torch.int32, (min_pages.numel(),), device)
+
+
+def _expect_out(out, out_dtype, shape, device):
+    import torch
+    dt = torch.float32 if out_dtype == SPARROW_OUT_F32 else torch.bfloat16
+    _expect(out, "out", dt, shape, device)
+
+
 # ------------------------------------------------------------------ tensor-level wrappers
 def page_meta_update(k_cache, block_table, seq_lens, meta, first_pos=None, shape=None,
                      landmark=SPARROW_LANDMARK_MINMAX):
     """Rebuild (first_pos None) or update the page metadata in ``meta`` (in place)."""
+    import torch
     _require_device(k_cache)
+    dev = k_cache.device
+    if k_cache.dim() != 4 or block_table.dim() != 2:
+        raise ValueError("k_cache must be [P][Hkv][ps][D], block_table [B][M]")
+    P, Hkv, ps, D = k_cache.shape
+    B, M = block_table.shape
+    _expect(k_cache, "k_cache", torch.bfloat16, (P, Hkv, ps, D), dev)
+    _expect(block_table, "block_table", torch.int32, (B, M), dev)
+    _expect(seq_lens, "seq_lens", torch.int32, (B,), dev)
+    if first_pos is not None:
+        _expect(first_pos, "first_pos", torch.int32, (B,), dev)
+    _expect_meta(meta, P, Hkv, D, landmark, dev)
     if shape is None:
-        P, Hkv, ps, D = k_cache.shape
-        shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D,
-                           landmark=landmark)
+        shape = make_shape(B, Hkv, Hkv, ps, M, P, D, landmark=landmark)
     rc = sparrow_page_meta_update(shape, _ptr(k_cache), _ptr(block_table), _ptr(seq_lens),
                                   _ptr(first_pos), _ptr(meta), _stream(k_cache.device))
     _check("sparrow_page_meta_update", rc)
@@ -302,10 +373,21 @@ def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta,
               landmark=SPARROW_LANDMARK_MINMAX):
     """Write token ``seq_lens[b] - 1`` of every sequence into the caches and update the
     metadata of its page (all in place)."""
+    import torch
     _require_device(k_cache)
+    dev = k_cache.device
+    if k_cache.dim() != 4 or block_table.dim() != 2:
+        raise ValueError("k_cache must be [P][Hkv][ps][D], block_table [B][M]")
     P, Hkv, ps, D = k_cache.shape
-    shape = make_shape(block_table.shape[0], Hkv, Hkv, ps, block_table.shape[1], P, D,
-                       landmark=landmark)
+    B, M = block_table.shape
+    _expect(k_cache, "k_cache", torch.bfloat16, (P, Hkv, ps, D), dev)
+    _expect(v_cache, "v_cache", torch.bfloat16, (P, Hkv, ps, D), dev)
+    _expect(block_table, "block_table", torch.int32, (B, M), dev)
+    _expect(seq_lens, "seq_lens", torch.int32, (B,), dev)
+    _expect(k_new, "k_new", torch.bfloat16, (B, Hkv, D), dev)
+    _expect(v_new, "v_new", torch.bfloat16, (B, Hkv, D), dev)
+    _expect_meta(meta, P, Hkv, D, landmark, dev)
+    shape = make_shape(B, Hkv, Hkv, ps, M, P, D, landmark=landmark)
     rc = sparrow_append_kv(shape, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
                            _ptr(block_table), _ptr(seq_lens), _ptr(meta), _stream(k_cache.device))
     _check("sparrow_append_kv", rc)
@@ -317,16 +399,26 @@ def page_score_topk(q, meta, block_table, seq_lens, k_cache_shape, min_pages, fr
     """Scores, budgets and top-k page lists.  Returns (k [B] int32, idx [B][Hkv][k_max] int32)."""
     import torch
     _require_device(q)
+    dev = q.device
     P, Hkv, ps, D = k_cache_shape
-    shape = make_shape(q.shape[0], q.shape[1], Hkv, ps, block_table.shape[1], P, D,
-                       landmark=landmark)
+    if q.dim() != 3 or block_table.dim() != 2:
+        raise ValueError("q must be [B][Hq][D], block_table [B][M]")
+    B, Hq, _ = q.shape
+    M = block_table.shape[1]
+    _expect(q, "q", torch.bfloat16, (B, Hq, D), dev)
+    _expect(block_table, "block_table", torch.int32, (B, M), dev)
+    _expect(seq_lens, "seq_lens", torch.int32, (B,), dev)
+    _expect_meta(meta, P, Hkv, D, landmark, dev)
+    _expect_tables(min_pages, frac_num, dev)
+    shape = make_shape(B, Hq, Hkv, ps, M, P, D, landmark=landmark)
     sched = Schedule(int(bin_tokens), int(min_pages.numel()), _ptr(min_pages), _ptr(frac_num),
                      int(frac_den), int(sink_pages), int(local_pages))
-    dev = q.device
     if out_k is None:
-        out_k = torch.empty(q.shape[0], dtype=torch.int32, device=dev)
+        out_k = torch.empty(B, dtype=torch.int32, device=dev)
     if out_idx is None:
-        out_idx = torch.empty((q.shape[0], Hkv, int(k_max)), dtype=torch.int32, device=dev)
+        out_idx = torch.empty((B, Hkv, int(k_max)), dtype=torch.int32, device=dev)
+    _expect(out_k, "out_k", torch.int32, (B,), dev)
+    _expect(out_idx, "out_idx", torch.int32, (B, Hkv, int(k_max)), dev)
     need = sparrow_workspace_size(shape, int(k_max), SPARROW_OP_SCORE_TOPK)
     if workspace is None:
         workspace = _workspace(need, dev)
@@ -341,13 +433,18 @@ def sparse_decode_attn(q, k_cache, v_cache, block_table, seq_lens, k, idx, scale
                        out_dtype=SPARROW_OUT_F32, workspace=None):
     """Attention over the selected pages.  Returns out [B][Hq][D] (fp32 or bf16)."""
     import torch
-    _require_device(q)
-    shape = shape_of(q, k_cache, block_table)
+    B, Hq, Hkv, ps, D, P, M = _expect_cache(q, k_cache, v_cache, block_table, seq_lens)
+    if idx.dim() != 3:
+        raise ValueError("idx must be [B][Hkv][k_max]")
     k_max = int(idx.shape[2])
+    _expect(k, "k", torch.int32, (B,), q.device)
+    _expect(idx, "idx", torch.int32, (B, Hkv, k_max), q.device)
+    shape = shape_of(q, k_cache, block_table)
     scale = 1.0 / math.sqrt(q.shape[2]) if scale is None else scale
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32 if out_dtype == SPARROW_OUT_F32
                           else torch.bfloat16, device=q.device)
+    _expect_out(out, out_dtype, (B, Hq, D), q.device)
     need = sparrow_workspace_size(shape, k_max, SPARROW_OP_SPARSE_ATTN)
     if workspace is None:
         workspace = _workspace(need, q.device)
@@ -364,12 +461,13 @@ def dense_decode_attn(q, k_cache, v_cache, block_table, seq_lens, scale=None, ou
                       out_dtype=SPARROW_OUT_F32, workspace=None):
     """Dense paged decode attention.  Returns out [B][Hq][D] (fp32 or bf16)."""
     import torch
-    _require_device(q)
+    B, Hq, Hkv, ps, D, P, M = _expect_cache(q, k_cache, v_cache, block_table, seq_lens)
     shape = shape_of(q, k_cache, block_table)
     scale = 1.0 / math.sqrt(q.shape[2]) if scale is None else scale
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32 if out_dtype == SPARROW_OUT_F32
                           else torch.bfloat16, device=q.device)
+    _expect_out(out, out_dtype, (B, Hq, D), q.device)
     need = sparrow_workspace_size(shape, 0, SPARROW_OP_DENSE_ATTN)
     if workspace is None:
         workspace = _workspace(need, q.device)
@@ -393,8 +491,12 @@ def acceptance_rate(target, draft, inv_temperature=1.0, alpha=None):
     T, V = target.shape
     if not (target.is_contiguous() and draft.is_contiguous()):
         raise ValueError("logit rows must be contiguous")
+    _require_device(draft)
+    if draft.device != target.device:
+        raise ValueError("target and draft logits must be on one device")
     if alpha is None:
         alpha = torch.empty(T, dtype=torch.float32, device=target.device)
+    _expect(alpha, "alpha", torch.float32, (T,), target.device)
     _check("sparrow_acceptance_rate", sparrow_acceptance_rate(
         T, V, dt, _ptr(target), _ptr(draft), float(inv_temperature), _ptr(alpha),
         _stream(target.device)))
@@ -405,9 +507,15 @@ def acceptance_rate_topk(lp_target, lp_draft, alpha=None):
     """Top-K approximation from log-probabilities ``[T][K]`` (fp32).  Returns alpha ``[T]``."""
     import torch
     _require_device(lp_target)
+    if lp_target.dim() != 2:
+        raise ValueError("log-probabilities must be [T][K]")
     T, K = lp_target.shape
+    dev = lp_target.device
+    _expect(lp_target, "lp_target", torch.float32, (T, K), dev)
+    _expect(lp_draft, "lp_draft", torch.float32, (T, K), dev)
     if alpha is None:
-        alpha = torch.empty(T, dtype=torch.float32, device=lp_target.device)
+        alpha = torch.empty(T, dtype=torch.float32, device=dev)
+    _expect(alpha, "alpha", torch.float32, (T,), dev)
     _check("sparrow_acceptance_rate_topk", sparrow_acceptance_rate_topk(
         T, K, _ptr(lp_target), _ptr(lp_draft), _ptr(alpha), _stream(lp_target.device)))
     return alpha
@@ -418,6 +526,8 @@ def tail_stats(alpha, positions, bin_tokens, n_bins, percentile=5.0):
     import torch
     _require_device(alpha)
     dev = alpha.device
+    _expect(alpha, "alpha", torch.float32, (alpha.numel(),), dev)
+    _expect(positions, "positions", torch.int32, (alpha.numel(),), dev)
     q = torch.empty(n_bins, dtype=torch.float64, device=dev)
     m = torch.empty(n_bins, dtype=torch.float64, device=dev)
     c = torch.empty(n_bins, dtype=torch.int64, device=dev)
@@ -433,8 +543,11 @@ def stream_read(buf, checksum=None):
     ``checksum`` when given, else to a new zero)."""
     import torch
     _require_device(buf)
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
     if checksum is None:
         checksum = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    _expect(checksum, "checksum", torch.int32, (1,), buf.device)
     _check("sparrow_stream_read", sparrow_stream_read(
         _ptr(buf), buf.numel() * buf.element_size(), _ptr(checksum), _stream(buf.device)))
     return checksum
@@ -450,7 +563,9 @@ class SparseDecodeStep:
                  frac_den, bin_tokens, k_max, scale=None, landmark=SPARROW_LANDMARK_MINMAX,
                  sink_pages=0, local_pages=0):
         import torch
-        _require_device(q)
+        B, Hq, Hkv, ps, D, P, M = _expect_cache(q, k_cache, v_cache, block_table, seq_lens)
+        _expect_meta(meta, P, Hkv, D, landmark, q.device)
+        _expect_tables(min_pages, frac_num, q.device)
         self.q, self.k_cache, self.v_cache = q, k_cache, v_cache
         self.block_table, self.seq_lens, self.meta = block_table, seq_lens, meta
         self.shape = shape_of(q, k_cache, block_table, landmark=landmark)
@@ -476,15 +591,31 @@ class SparseDecodeStep:
     # Every method takes an optional ``seq_lens`` tensor that replaces the one given at
     # construction for that call (a decode loop advances the lengths step by step).
     def _lens(self, seq_lens):
-        return _ptr(self.seq_lens if seq_lens is None else seq_lens)
+        import torch
+        if seq_lens is None:
+            return _ptr(self.seq_lens)
+        _expect(seq_lens, "seq_lens", torch.int32, tuple(self.seq_lens.shape), self.q.device)
+        return _ptr(seq_lens)
+
+    def _rows(self, k_new, v_new):
+        """The decoded token's rows: bf16 [B][Hkv][D] each."""
+        import torch
+        want = (self.q.shape[0], self.k_cache.shape[1], self.q.shape[2])
+        _expect(k_new, "k_new", torch.bfloat16, want, self.q.device)
+        _expect(v_new, "v_new", torch.bfloat16, want, self.q.device)
 
     def meta_update(self, first_pos, stream, seq_lens=None):
+        import torch
+        if first_pos is not None:
+            _expect(first_pos, "first_pos", torch.int32, tuple(self.seq_lens.shape),
+                    self.q.device)
         _check("sparrow_page_meta_update", sparrow_page_meta_update(
             self.shape, _ptr(self.k_cache), _ptr(self.block_table), self._lens(seq_lens),
             _ptr(first_pos), _ptr(self.meta), stream))
 
     def append(self, k_new, v_new, stream, seq_lens=None):
         """Write the decoded token's K/V rows and update its page's metadata."""
+        self._rows(k_new, v_new)
         _check("sparrow_append_kv", sparrow_append_kv(
             self.shape, _ptr(k_new), _ptr(v_new), _ptr(self.k_cache), _ptr(self.v_cache),
             _ptr(self.block_table), self._lens(seq_lens), _ptr(self.meta), stream))
@@ -497,6 +628,7 @@ class SparseDecodeStep:
 
     def append_score_topk(self, k_new, v_new, stream, seq_lens=None):
         """Append the decoded token (k_new/v_new [B][Hkv][D]) and select pages, fused."""
+        self._rows(k_new, v_new)
         _check("sparrow_append_score_topk", sparrow_append_score_topk(
             self.shape, _ptr(self.q), _ptr(k_new), _ptr(v_new), _ptr(self.k_cache),
             _ptr(self.v_cache), _ptr(self.meta), _ptr(self.block_table), self._lens(seq_lens),
@@ -514,6 +646,10 @@ class SparseDecodeStep:
         """The whole step in one call (sparrow_decode_step): append the decoded token
         (k_new/v_new [B][Hkv][D], or both None for no append), select pages, attend; the
         same results as append_score_topk (or score_topk) followed by attend."""
+        if (k_new is None) != (v_new is None):
+            raise ValueError("k_new and v_new are both given or both None")
+        if k_new is not None:
+            self._rows(k_new, v_new)
         _check("sparrow_decode_step", sparrow_decode_step(
             self.shape, _ptr(self.q), _ptr(k_new), _ptr(v_new), _ptr(self.k_cache),
             _ptr(self.v_cache), _ptr(self.meta), _ptr(self.block_table), self._lens(seq_lens),
