@@ -240,6 +240,34 @@ def test_duplicated_pages_at_the_cut():
     assert r["gpu"]["idx"][0, 0, :2].tolist() == [10, 50]
 
 
+@pytest.mark.parametrize("perturb", [False, True])
+def test_many_pages_in_the_threshold_digit(perturb):
+    """100 copies of one boosted page, budget 50: the radix select's threshold digit holds
+    many keys pass after pass - down to the last bit for identical copies (ties to the lower
+    index), or until the copies' scores, nudged apart in one channel each, separate.  With 8
+    units (512-thread top-k) and with the batch repeated to 1024 units (256-thread top-k),
+    which must select alike."""
+    log(f"case many pages in the threshold digit, perturbed {perturb}")
+    inp = small_inputs(2, 8, 16, (3000,), seed=14, schedule=W.fixed_budget(50))
+    bt = inp.block_table.cpu().numpy()
+    src = int(bt[0, 150])
+    inp.k_cache[src] = (inp.k_cache[src].float() * 3).to(torch.bfloat16)
+    for j, p in enumerate(range(20, 120)):
+        dst = int(bt[0, p])
+        inp.k_cache[dst] = inp.k_cache[src]
+        if perturb:
+            c = j % 128
+            v = inp.k_cache[dst, :, :, c].float()
+            inp.k_cache[dst, :, :, c] = (v * (1.0 + (j + 1) / 512.0)).to(torch.bfloat16)
+    small = full_check(inp)
+    if not perturb:
+        for h in range(8):   # the 50 lowest of the 101 identical pages
+            assert small["gpu"]["idx"][0, h, :50].tolist() == list(range(20, 70))
+    big = full_check(replicated(inp, 128))
+    for r in range(128):
+        assert np.array_equal(big["gpu"]["idx"][r:r + 1], small["gpu"]["idx"])
+
+
 def test_signed_zero_keys_and_scores():
     log("case signed zeros")
     inp = small_inputs(2, 2, 16, (900, 333), seed=13, schedule=W.fixed_budget(6))
