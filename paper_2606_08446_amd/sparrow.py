@@ -361,6 +361,8 @@ def page_meta_update(k_cache, block_table, seq_lens, meta, first_pos=None, shape
     if first_pos is not None:
         _expect(first_pos, "first_pos", torch.int32, (B,), dev)
     _expect_meta(meta, P, Hkv, D, landmark, dev)
+    if B == 0:   # nothing to launch (an empty tensor's data pointer is null)
+        return meta
     if shape is None:
         shape = make_shape(B, Hkv, Hkv, ps, M, P, D, landmark=landmark)
     rc = sparrow_page_meta_update(shape, _ptr(k_cache), _ptr(block_table), _ptr(seq_lens),
@@ -387,6 +389,8 @@ def append_kv(k_new, v_new, k_cache, v_cache, block_table, seq_lens, meta,
     _expect(k_new, "k_new", torch.bfloat16, (B, Hkv, D), dev)
     _expect(v_new, "v_new", torch.bfloat16, (B, Hkv, D), dev)
     _expect_meta(meta, P, Hkv, D, landmark, dev)
+    if B == 0:
+        return
     shape = make_shape(B, Hkv, Hkv, ps, M, P, D, landmark=landmark)
     rc = sparrow_append_kv(shape, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
                            _ptr(block_table), _ptr(seq_lens), _ptr(meta), _stream(k_cache.device))
@@ -419,6 +423,8 @@ def page_score_topk(q, meta, block_table, seq_lens, k_cache_shape, min_pages, fr
         out_idx = torch.empty((B, Hkv, int(k_max)), dtype=torch.int32, device=dev)
     _expect(out_k, "out_k", torch.int32, (B,), dev)
     _expect(out_idx, "out_idx", torch.int32, (B, Hkv, int(k_max)), dev)
+    if B == 0:
+        return out_k, out_idx
     need = sparrow_workspace_size(shape, int(k_max), SPARROW_OP_SCORE_TOPK)
     if workspace is None:
         workspace = _workspace(need, dev)
@@ -445,6 +451,8 @@ def sparse_decode_attn(q, k_cache, v_cache, block_table, seq_lens, k, idx, scale
         out = torch.empty(q.shape, dtype=torch.float32 if out_dtype == SPARROW_OUT_F32
                           else torch.bfloat16, device=q.device)
     _expect_out(out, out_dtype, (B, Hq, D), q.device)
+    if B == 0:
+        return out
     need = sparrow_workspace_size(shape, k_max, SPARROW_OP_SPARSE_ATTN)
     if workspace is None:
         workspace = _workspace(need, q.device)
@@ -468,6 +476,8 @@ def dense_decode_attn(q, k_cache, v_cache, block_table, seq_lens, scale=None, ou
         out = torch.empty(q.shape, dtype=torch.float32 if out_dtype == SPARROW_OUT_F32
                           else torch.bfloat16, device=q.device)
     _expect_out(out, out_dtype, (B, Hq, D), q.device)
+    if B == 0:
+        return out
     need = sparrow_workspace_size(shape, 0, SPARROW_OP_DENSE_ATTN)
     if workspace is None:
         workspace = _workspace(need, q.device)
@@ -497,6 +507,8 @@ def acceptance_rate(target, draft, inv_temperature=1.0, alpha=None):
     if alpha is None:
         alpha = torch.empty(T, dtype=torch.float32, device=target.device)
     _expect(alpha, "alpha", torch.float32, (T,), target.device)
+    if T == 0:   # nothing to launch (an empty tensor's data pointer is null)
+        return alpha
     _check("sparrow_acceptance_rate", sparrow_acceptance_rate(
         T, V, dt, _ptr(target), _ptr(draft), float(inv_temperature), _ptr(alpha),
         _stream(target.device)))
@@ -516,6 +528,8 @@ def acceptance_rate_topk(lp_target, lp_draft, alpha=None):
     if alpha is None:
         alpha = torch.empty(T, dtype=torch.float32, device=dev)
     _expect(alpha, "alpha", torch.float32, (T,), dev)
+    if T == 0:
+        return alpha
     _check("sparrow_acceptance_rate_topk", sparrow_acceptance_rate_topk(
         T, K, _ptr(lp_target), _ptr(lp_draft), _ptr(alpha), _stream(lp_target.device)))
     return alpha

@@ -143,6 +143,24 @@ def test_acceptance_around_the_on_chip_boundaries(dtype, vi, off):
         assert err.max() <= ALPHA_TOL
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_acceptance_is_deterministic_and_takes_no_tokens(dtype):
+    """Two runs give the same bits (fixed reduction order), the rate of a token does not
+    depend on the others in the launch, and zero tokens enqueue nothing."""
+    log(f"case acceptance determinism {dtype}")
+    li = W.generate_logits(W.small_logits(T=9, V=70001, seed=5, dtype=dtype), DEV)
+    a = S.acceptance_rate(li.target, li.draft, 0.9)
+    b = S.acceptance_rate(li.target, li.draft, 0.9)
+    one = S.acceptance_rate(li.target[4:5], li.draft[4:5], 0.9)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    assert torch.equal(a[4:5].view(torch.int32), one.view(torch.int32))
+    keep = torch.full((3,), -5.0, device=DEV)
+    S.acceptance_rate(li.target[:0], li.draft[:0], 1.0, alpha=keep[:0])
+    torch.cuda.synchronize()
+    assert (keep == -5.0).all()
+
+
 def test_acceptance_unaligned_row_starts():
     # views whose rows start off a 16-byte boundary (both rows in the same phase)
     li = W.generate_logits(W.small_logits(T=9, V=2051, seed=4), DEV)

@@ -118,3 +118,29 @@ def test_acceptance_wrappers_check_their_buffers():
     q, m, c = S.tail_stats(alpha, li.positions, 2048, 20)
     torch.cuda.synchronize()
     assert int(c.sum()) == 5
+
+
+def test_empty_batches_launch_nothing():
+    """A batch of no sequences (or no tokens) returns at once: torch gives an empty tensor a
+    null data pointer, which the C ABI would refuse, and there is nothing to compute."""
+    log("case wrapper checks: empty batches")
+    q = torch.zeros((0, 4, 128), dtype=torch.bfloat16, device=DEV)
+    kc = torch.zeros((5, 2, 16, 128), dtype=torch.bfloat16, device=DEV)
+    bt = torch.zeros((0, 3), dtype=torch.int32, device=DEV)
+    lens = torch.zeros((0,), dtype=torch.int32, device=DEV)
+    meta = S.new_meta(5, 2, DEV)
+    S.page_meta_update(kc, bt, lens, meta)
+    S.append_kv(torch.zeros((0, 2, 128), dtype=torch.bfloat16, device=DEV),
+                torch.zeros((0, 2, 128), dtype=torch.bfloat16, device=DEV), kc, kc.clone(), bt,
+                lens, meta)
+    tables = torch.ones(1, dtype=torch.int32, device=DEV)
+    k, idx = S.page_score_topk(q, meta, bt, lens, tuple(kc.shape), tables, tables.clone(), 1,
+                               2048, 4)
+    assert k.shape == (0,) and idx.shape == (0, 2, 4)
+    assert S.sparse_decode_attn(q, kc, kc, bt, lens, k, idx).shape == (0, 4, 128)
+    assert S.dense_decode_attn(q, kc, kc, bt, lens).shape == (0, 4, 128)
+    logits = torch.zeros((0, 100), device=DEV)
+    assert S.acceptance_rate(logits, logits).shape == (0,)
+    assert S.acceptance_rate_topk(torch.zeros((0, 20), device=DEV),
+                                  torch.zeros((0, 20), device=DEV)).shape == (0,)
+    torch.cuda.synchronize()
