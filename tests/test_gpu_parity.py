@@ -68,6 +68,11 @@ SWEEP = [
     (6, 3, 64, (4000, 129, 7000), W.fraction_budget(1, 4)),
     (7, 2, 128, (2600, 257), W.fraction_budget(1, 2)),
     (12, 1, 32, (6000, 31, 1900), W.rising_permille(2048, 2048, 8192, 40, 200)),
+    # more KV heads than one scoring workgroup takes (8): two and four head blocks, the
+    # last partial
+    (1, 16, 16, (3000, 70, 1), W.fraction_budget(1, 6)),
+    (2, 20, 32, (2500, 900), W.fraction_budget(1, 5)),
+    (1, 32, 64, (5000, 129), W.fixed_budget(9)),
 ]
 
 
