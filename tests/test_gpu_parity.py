@@ -287,6 +287,42 @@ def test_signed_zero_keys_and_scores():
     full_check(inp)
 
 
+@pytest.mark.parametrize("scale", [0.03, 0.25, 0.6])
+@pytest.mark.parametrize("units", ["few", "many"])
+def test_softmax_scale_is_applied(scale, units):
+    """Sparse and dense attention at softmax scales other than 1/sqrt(128), on the
+    one-workgroup-per-unit path (8 units) and the streaming path (320 units), against the
+    oracle at the same scale; the whole-step call takes the scale as the separate calls do."""
+    B, Hkv = (2, 4) if units == "few" else (40, 8)
+    lengths = tuple(int(x) for x in np.random.default_rng(31).integers(300, 3000, size=B))
+    log(f"case softmax scale {scale}, {B * Hkv} units")
+    inp = small_inputs(2, Hkv, 16, lengths, seed=32, schedule=W.fixed_budget(20))
+    h = host(inp)
+    meta = torch.zeros((inp.num_phys_pages, Hkv, 2, 128), dtype=torch.bfloat16, device=DEV)
+    S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta)
+    s = inp.workload.schedule
+    k, idx = S.page_score_topk(inp.q, meta, inp.block_table, inp.seq_lens, inp.k_cache.shape,
+                               inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, 20)
+    out_s = S.sparse_decode_attn(inp.q, inp.k_cache, inp.v_cache, inp.block_table,
+                                 inp.seq_lens, k, idx, scale)
+    out_d = S.dense_decode_attn(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+                                scale)
+    step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+                              meta, inp.min_pages, inp.frac_num, s.frac_den, s.bin_tokens, 20,
+                              scale=scale)
+    whole = step.decode_step(None, None, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    gk, gidx = k.cpu().numpy(), idx.cpu().numpy()
+    check_out(out_s.cpu().numpy().astype(np.float64),
+              oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], scale, gk, gidx),
+              f"sparse, scale {scale}")
+    check_out(out_d.cpu().numpy().astype(np.float64),
+              oracle.attention(h["q"], h["k"], h["v"], h["bt"], h["lens"], scale),
+              f"dense, scale {scale}")
+    assert torch.equal(step.idx, idx)
+    assert torch.equal(whole.view(torch.int32), out_s.view(torch.int32))
+
+
 # ---------------------------------------------------------------------------------- metadata
 @pytest.mark.parametrize("step", [1, 9, 40])
 def test_meta_incremental_update_equals_rebuild(step):
