@@ -33,7 +33,9 @@
  *    [0, num_phys_pages) marks an absent page - no kernel reads or writes that
  *    physical page; scoring sees zero metadata for it (score 0), attention
  *    leaves its tokens out, and an append to it writes nothing - and page
- *    indices, lengths and budgets are clamped to what the shape allows.
+ *    indices, lengths and budgets are clamped to what the shape allows (a
+ *    negative length is an empty sequence; one beyond max_pages_per_seq *
+ *    page_size tokens counts as that many, and its token is not appended).
  *  - bf16 tensors are IEEE bfloat16 bit patterns.  NaN inputs are not supported.
  *  - Alignment: q, k_cache, v_cache, meta, out and workspace start on a 16-byte
  *    boundary and the int32 arrays on a 4-byte boundary (any hipMalloc or PyTorch

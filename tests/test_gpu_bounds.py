@@ -240,3 +240,44 @@ def test_block_table_entries_past_the_sequence_do_not_matter():
     got = run(torch.as_tensor(bt, device=DEV))
     for x, y in zip(got, ref):
         assert torch.equal(x, y)
+
+
+@pytest.mark.parametrize("whole", [False, True])
+def test_negative_lengths_count_as_empty(whole):
+    """A negative length is an empty sequence, as 0 is: no pages, budget 0, a zero output
+    row, no append; the other sequences are unaffected (separate calls and the whole-step
+    call, on the one-kernel and the streaming path)."""
+    log(f"case negative lengths, whole-step call {whole}")
+    lengths = (900, 0, 2500, 0, 40)
+    w = W.small(B=5, Hq=4, Hkv=2, ps=16, lengths=lengths, seed=23, schedule=W.fixed_budget(12))
+    outs = []
+    for neg in (False, True):
+        inp = W.generate(w, DEV, lengths=list(lengths))
+        if neg:
+            inp.seq_lens[1] = -7
+            inp.seq_lens[3] = -(2**31)
+        meta = S.new_meta(inp.num_phys_pages, 2, DEV)
+        S.page_meta_update(inp.k_cache, inp.block_table, inp.seq_lens, meta)
+        s = w.schedule
+        step = S.SparseDecodeStep(inp.q, inp.k_cache, inp.v_cache, inp.block_table,
+                                  inp.seq_lens, meta, inp.min_pages, inp.frac_num, s.frac_den,
+                                  s.bin_tokens, 12)
+        g = torch.Generator(device=DEV)
+        g.manual_seed(24)
+        kn = torch.randn((5, 2, 128), generator=g, device=DEV).to(torch.bfloat16)
+        vn = torch.randn((5, 2, 128), generator=g, device=DEV).to(torch.bfloat16)
+        stream = torch.cuda.current_stream().cuda_stream
+        if whole:
+            step.decode_step(kn, vn, stream)
+        else:
+            step.append_score_topk(kn, vn, stream)
+            step.attend(stream)
+        dense = S.dense_decode_attn(inp.q, inp.k_cache, inp.v_cache, inp.block_table,
+                                    inp.seq_lens, SCALE)
+        torch.cuda.synchronize()
+        outs.append((step.k.cpu().numpy(), step.idx.cpu().numpy(), step.out.cpu().numpy(),
+                     dense.cpu().numpy(), W.bf16_bits(inp.k_cache), W.bf16_bits(meta)))
+    for name, a, b in zip(("k", "idx", "out", "dense", "k_cache", "meta"), outs[0], outs[1]):
+        np.testing.assert_array_equal(a, b, err_msg=name)
+    assert outs[1][0][1] == 0 and outs[1][0][3] == 0
+    assert (outs[1][2][1] == 0).all() and (outs[1][3][3] == 0).all()
